@@ -1,0 +1,193 @@
+#!/usr/bin/env python3
+"""Throughput of the compressed se_a descriptor (DP Compress, arXiv:2107.02103).
+
+One step = one forward (T, D) plus one backward (dE/dR~) pass of the HIP
+kernels over the whole workload, inputs resident in HBM.  Default workload:
+Cu-like fcc 64^3 supercell, 1,048,576 atoms, r_c 8.0 A, sel 512, embedding
+1->25->50->100, M' = 16, float64.
+
+Prints one JSON line: neighbour pairs/s (whole job), the fraction of the
+FP64 vector FMA peak reached with the algorithmic FLOP count
+(5,400 per valid pair + 12,800 per atom), the roofline of the dominant kernel
+(HIP events on the launch stream) and the plain C oracle timed on this host's
+cores on a bounded sample of the same workload.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "neighbor-pairs/s fwd+bwd compressed se_a (fp64) + % of FP64 vector FMA peak"
+PEAK_TFLOPS = {"f64": 78.6, "f32": 157.3, "f32acc64": 157.3}   # MI355X vector peaks
+FLOP_PAIR_FWD, FLOP_PAIR_BWD, FLOP_ATOM = 1800.0, 3600.0, 12800.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    p = os.path.join(ROOT, "paper_2107_02103_amd", "csrc", "dpc_se_a.hip")
+    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+
+
+def hbm_traffic(cfg_name, kernel):
+    """HBM bytes per launch from the committed rocprofv3 --pmc summary, if it
+    was taken on the current kernel source; else None."""
+    p = os.path.join(ROOT, "profiles", f"pmc_{kernel}_{cfg_name}.json")
+    if not os.path.exists(p):
+        return None
+    d = json.load(open(p))
+    if d.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(x, seconds):
+    """The C oracle (plain loops, OpenMP over atoms) on the first atoms of the
+    workload, in chunks, until `seconds` of wall time are used."""
+    import numpy as np
+    from oracle import cref
+    from oracle.table import build_tables
+    c = x.cfg
+    pb = cref.Problem(x.em, x.nlist, x.atype, build_tables(x), c.sel, c.m2)
+    n = x.nlist.shape[0]
+    chunk = 512
+    done, pairs = 0, 0
+    t0 = time.perf_counter()
+    while done < n and time.perf_counter() - t0 < seconds:
+        i1 = min(n, done + chunk)
+        pb.forward(done, i1)
+        pb.backward(x.dT[done:i1], done, i1)
+        pairs += int((x.nlist[done:i1] >= 0).sum())
+        done = i1
+    dt = time.perf_counter() - t0
+    cpu = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": pairs / dt, "unit": "pairs/s", "cores": cref.num_threads(), "kind": "oracle",
+            "sample": f"atoms 0..{done - 1} of {n} ({pairs} valid pairs), fwd+bwd, {dt:.1f} s, {cpu}"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="3", help="workload index 0..4 or name (default 3: cu1m)")
+    ap.add_argument("--dtype", default=None, choices=[None, "f64", "f32", "f32acc64"])
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the descriptor kernel "
+              "shards by atoms with no exchange, so multi-GPU throughput is not measured here.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2107_02103_amd as P
+    from synth import make_inputs
+    from synth.configs import get_config
+
+    key = int(args.config) if args.config.isdigit() else args.config
+    cfg = get_config(key)
+    dtype = args.dtype or cfg.dtype
+    mode = {"f64": P.DPC_F64, "f32": P.DPC_F32, "f32acc64": P.DPC_F32_ACC64}[dtype]
+    store = np.float64 if dtype == "f64" else np.float32
+
+    t = time.perf_counter()
+    log(f"[bench] generating {cfg.name} ({cfg.natoms} atoms, sel {cfg.sel})")
+    x = make_inputs(cfg)
+    atoms, pairs = cfg.natoms, x.n_valid
+    log(f"[bench] inputs ready in {time.perf_counter() - t:.1f} s: {pairs} valid pairs")
+
+    op = P.SeATab(x.nets, x.lo, x.L1, x.L2, cfg.d1, cfg.d2, cfg.sel, cfg.m2, dtype=mode)
+    em = torch.from_numpy(x.em.astype(store, copy=False)).cuda()
+    nl = torch.from_numpy(x.nlist).cuda()
+    at = torch.from_numpy(x.atype).cuda()
+    dT = torch.from_numpy(x.dT.astype(store, copy=False)).cuda()
+    tacc = torch.float32 if dtype == "f32" else torch.float64
+    T = torch.empty((atoms, cfg.m1, 4), dtype=tacc, device="cuda")
+    D = torch.empty((atoms, cfg.m1, cfg.m2), dtype=tacc, device="cuda")
+    dR = torch.empty((atoms, cfg.nnei, 4), dtype=tacc, device="cuda")
+    torch.cuda.synchronize()
+    log(f"[bench] resident on {torch.cuda.get_device_name(0)}")
+
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        for _ in range(args.warmup):
+            op.forward(em, nl, at, T, D, stream=s)
+            op.backward(em, nl, at, dT, dR, stream=s)
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+                torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        t0 = time.perf_counter()
+        for e0, e1, e2 in evs:
+            e0.record(s)
+            op.forward(em, nl, at, T, D, stream=s)
+            e1.record(s)
+            op.backward(em, nl, at, dT, dR, stream=s)
+            e2.record(s)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+    fwd_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in evs]))
+    bwd_ms = float(np.mean([b.elapsed_time(c) for _, b, c in evs]))
+    log(f"[bench] {args.steps} steps in {wall:.3f} s: fwd {fwd_ms:.3f} ms, bwd {bwd_ms:.3f} ms")
+
+    flop_fwd = FLOP_PAIR_FWD * pairs + FLOP_ATOM * atoms
+    flop_bwd = FLOP_PAIR_BWD * pairs
+    step_s = wall / args.steps
+    peak = PEAK_TFLOPS[dtype]
+    tflops = (flop_fwd + flop_bwd) / step_s / 1e12
+    dom = "se_a_bwd_kernel" if bwd_ms >= fwd_ms else "se_a_fwd_kernel"
+    dom_ms = max(bwd_ms, fwd_ms)
+    dom_flop = flop_bwd if bwd_ms >= fwd_ms else flop_fwd
+    achieved = dom_flop / (dom_ms * 1e-3) / 1e12
+    out = {
+        "metric": METRIC,
+        "value": pairs * args.steps / wall,
+        "unit": "pairs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_s * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.kind} {cfg.ncell}^3 cells, {atoms} atoms, "
+                               f"rc {cfg.rc}, rcs {cfg.rcs}, sel {list(cfg.sel)}, "
+                               f"embedding {'-'.join(map(str, cfg.widths))}, M2 {cfg.m2}, "
+                               f"table stride {cfg.d1}/{cfg.d2}",
+                   "atoms": atoms, "valid_pairs": pairs, "nnei": cfg.nnei},
+        "tflops_algorithmic": tflops,
+        "frac_vector_peak": tflops / peak,
+        "fwd_ms": fwd_ms,
+        "bwd_ms": bwd_ms,
+        "roofline": {"bound": "alu", "kernel": dom, "achieved": achieved, "peak": peak,
+                     "unit": "TFLOP/s", "frac": achieved / peak,
+                     "traffic": hbm_traffic(cfg.name, dom)},
+    }
+    del T, D, dR, em, dT
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        log(f"[bench] cpu baseline (oracle) for ~{args.cpu_seconds:.0f} s")
+        out["cpu_baseline"] = cpu_baseline(x, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,147 @@
+/*
+ * dpc.h -- C ABI of the compressed se_a descriptor library (libdpc.so).
+ *
+ * DP Compress (Lu et al., arXiv:2107.02103), Sec. II: the embedding net
+ * G(s^) of the Deep Potential se_a descriptor is replaced by a table of
+ * piecewise fifth-order Hermite polynomials, and the product
+ * S_i = G_i^T R~_i (here called T_i, M1 x 4) is evaluated by one fused kernel
+ * that never materialises G and skips padded neighbours; then
+ * D_i = T_i (T_i<)^T (M1 x M2) with T_i< the first M2 rows of T_i.  The
+ * backward kernel maps dE/dT_i to dE/dR~_ij through the polynomial and its
+ * derivative, which is what forces need.
+ *
+ * Conventions
+ *  - All arrays are row-major and contiguous; sizes are element counts.
+ *  - "device" pointers are HIP device memory on the current device; "host"
+ *    pointers are ordinary host memory.  The library never allocates device
+ *    memory and keeps no global state: every buffer is owned by the caller.
+ *  - Kernels are enqueued on the given stream (a hipStream_t passed as
+ *    void*, NULL = the null stream) and the calls return without
+ *    synchronising.  Faults inside a kernel surface at the caller's next
+ *    synchronisation.
+ *  - Every argument is validated on the host before anything is launched;
+ *    on error nothing is launched and nothing is written.
+ *  - Return value: DPC_OK (0) or a negative DPC_E* code; dpc_strerror()
+ *    describes it.
+ */
+#ifndef DPC_H
+#define DPC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DPC_OK 0
+#define DPC_EINVAL -1   /* null pointer, bad size/shape, bad dtype, sel/nnei mismatch */
+#define DPC_ERANGE -2   /* bad table parameters: stride <= 0, L1 or L2 < 1, non-finite lo */
+#define DPC_EHIP -3     /* HIP runtime or launch error */
+#define DPC_ENOTSUP -4  /* supported but not implemented sizes (M1 > 256, ntypes > 8) */
+
+#define DPC_MAX_TYPES 8
+#define DPC_MAX_M1 256
+
+/* Arithmetic of the kernels.
+ *  DPC_F64        float64 table, R~, dE/dT, T, D and dE/dR~.
+ *  DPC_F32        float32 table, R~, dE/dT, T, D and dE/dR~, float32 arithmetic.
+ *  DPC_F32_ACC64  float32 table, R~ and dE/dT; polynomial evaluated in float32,
+ *                 T, D and dE/dR~ accumulated and stored in float64.          */
+typedef enum { DPC_F64 = 0, DPC_F32 = 1, DPC_F32_ACC64 = 2 } dpc_dtype;
+
+/* Tabulation range of one embedding net (one ordered type pair).
+ * Paper Sec. II: the input s^ is tabulated on [s^(r_c), s^(r_l)] with an
+ * equal step; here the main range [lo, x_up], x_up = lo + L1*d1, uses step d1
+ * and an extrapolation band [x_up, x_end], x_end = x_up + L2*d2, uses d2.
+ * Interval l < L1 covers [lo + l*d1, lo + (l+1)*d1); interval L1 + l covers
+ * [x_up + l*d2, x_up + (l+1)*d2).  Inputs below lo use interval 0 (t < 0);
+ * inputs at or beyond x_end take the value at x_end and zero derivative.
+ * `offset` is the element offset of this pair's coefficients inside the
+ * coefficient buffer; dpc_table_layout() fills it.                          */
+typedef struct {
+  double lo;
+  double d1;
+  double d2;
+  int64_t L1;
+  int64_t L2;
+  int64_t offset;
+} dpc_range;
+
+/* Embedding net of one type pair (host memory, read only).
+ * widths[0] must be 1; layer k maps widths[k] -> widths[k+1] with
+ * y_{k+1} = tanh(y_k W_k + b_k) (+ [y_k, y_k] when widths[k+1] = 2 widths[k],
+ * + y_k when widths[k+1] = widths[k]).  W[k] is [widths[k]][widths[k+1]].  */
+typedef struct {
+  int n_layers;
+  const int* widths;         /* [n_layers + 1] */
+  const double* const* W;    /* [n_layers] */
+  const double* const* b;    /* [n_layers] */
+} dpc_net;
+
+/* Human-readable text of a status code (static storage). */
+const char* dpc_strerror(int status);
+
+/* Text of the HIP error behind the calling thread's last DPC_EHIP status
+ * ("no error" if there was none). */
+const char* dpc_last_hip_error(void);
+
+/* Library version as 10000*major + 100*minor + patch. */
+int dpc_version(void);
+
+/* Coefficient layout for `npair` type pairs of width m1.
+ * In:  ranges[p].{lo,d1,d2,L1,L2}.  Out: ranges[p].offset (elements) and
+ * *total_bytes, the size of the coefficient buffer for `dtype` (DPC_F32 and
+ * DPC_F32_ACC64 store float32 coefficients).  The layout of one pair is
+ * [L1 + L2][6][m1]: for interval l, row q holds the coefficient of t^q of
+ * every channel, t = x - (left node of l).                                  */
+int dpc_table_layout(int npair, int m1, dpc_range* ranges, dpc_dtype dtype,
+                     size_t* total_bytes);
+
+/* Paper Sec. II, Eqs. for the constraints y, y', y'' at both nodes of each
+ * interval and the closed forms for a..f: tabulate `net` (m1 = last width)
+ * over `range` and write its [L1 + L2][6][m1] coefficients to `host_out`
+ * (host memory, float64 or float32 per `dtype`).  The first and second
+ * derivatives of the net are computed in forward mode in float64.          */
+int dpc_build_table(const dpc_net* net, const dpc_range* range, dpc_dtype dtype,
+                    void* host_out);
+
+/* Forward (paper Sec. II, the fused tabulate-and-contract kernel and D):
+ *   T_i[m][k] = sum over valid j of g_m^{a_i b_j}(R~_ij[0]) * R~_ij[k]
+ *   D_i[m][n] = sum_k T_i[m][k] * T_i[n][k],  n < m2
+ * Geometry: neighbour slot j of atom i belongs to block b_j (the first sel[0]
+ * slots are block 0, the next sel[1] block 1, ...), nnei = sum(sel); its
+ * table is pair a_i*ntypes + b_j with a_i = atype[i].  nlist[i][j] < 0 marks
+ * padding, which is skipped (it contributes exactly zero).
+ *   stream   hipStream_t as void*
+ *   sel      host [ntypes], ntypes <= DPC_MAX_TYPES
+ *   ranges   host [ntypes*ntypes], offsets from dpc_table_layout()
+ *   coeff    device, the concatenated tables (float64 or float32 per dtype)
+ *   atype    device int32 [nloc], values in [0, ntypes); an atom with another
+ *            value gets NaN outputs (nothing is read out of bounds)
+ *   nlist    device int32 [nloc][nnei]
+ *   em       device R~ [nloc][nnei][4] (float64 for DPC_F64, else float32)
+ *   T        device out [nloc][m1][4]   (float32 only for DPC_F32)
+ *   D        device out [nloc][m1][m2]  (float32 only for DPC_F32)
+ * Requires 1 <= m1 <= DPC_MAX_M1, 1 <= m2 <= m1.  nloc = 0 is a no-op.      */
+int dpc_se_a_tab_fwd(void* stream, dpc_dtype dtype, int nloc, int ntypes, const int* sel,
+                     int m1, int m2, const dpc_range* ranges, const void* coeff,
+                     const int* atype, const int* nlist, const void* em,
+                     void* T, void* D);
+
+/* Backward of T (forces need dE/dR~, paper Sec. II):
+ *   dE/dR~_ij[k] = sum_m dE/dT_i[m][k] g_m(x) + (k == 0) sum_m g'_m(x) w_m,
+ *   w_m = sum_k' dE/dT_i[m][k'] R~_ij[k'],  x = R~_ij[0],
+ * for valid j; padded rows are written as 0.
+ *   dE_dT    device [nloc][m1][4] (float64 for DPC_F64, else float32)
+ *   dE_dem   device out [nloc][nnei][4] (float32 only for DPC_F32)
+ * Other arguments as dpc_se_a_tab_fwd.                                      */
+int dpc_se_a_tab_bwd(void* stream, dpc_dtype dtype, int nloc, int ntypes, const int* sel,
+                     int m1, const dpc_range* ranges, const void* coeff,
+                     const int* atype, const int* nlist, const void* em,
+                     const void* dE_dT, void* dE_dem);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DPC_H */

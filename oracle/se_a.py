@@ -33,8 +33,11 @@ def _blocks(sel):
 def forward(em, nlist, atype, tables, sel, m2, atoms=None, with_abs=False):
     """T [n, M, 4] and D [n, M, m2] for the atoms ``atoms`` (default: all).
 
-    With ``with_abs`` also returns the abs-sum bounds
-    A_T[m][k] = sum_j |g_m R~_jk| and A_D = |T| |T<|^T used by the tolerances."""
+    With ``with_abs`` also returns the abs-sum bounds used by the tolerances:
+    A_T[m][k] = sum_j |g_m R~_jk| bounds the rounding of T (any summation
+    order), and A_D[m][n] = sum_k A_T[m][k] |T[n][k]| + |T[m][k]| A_T[n][k]
+    + |T[m][k] T[n][k]| bounds how an error of relative size eps in the terms
+    of T (eps * A_T) and in the products of D propagates into D."""
     nt = len(sel)
     atoms = np.arange(nlist.shape[0]) if atoms is None else np.asarray(atoms)
     M = tables[0].M
@@ -53,7 +56,9 @@ def forward(em, nlist, atype, tables, sel, m2, atoms=None, with_abs=False):
     D = T @ np.transpose(T[:, :m2, :], (0, 2, 1))
     if not with_abs:
         return T, D
-    AD = np.abs(T) @ np.transpose(np.abs(T[:, :m2, :]), (0, 2, 1))
+    aT = np.abs(T)
+    AD = (AT @ np.transpose(aT[:, :m2, :], (0, 2, 1)) + aT @ np.transpose(AT[:, :m2, :], (0, 2, 1))
+          + aT @ np.transpose(aT[:, :m2, :], (0, 2, 1)))
     return T, D, AT, AD
 
 

@@ -1,0 +1,191 @@
+"""ctypes binding of libdpc.so (see include/dpc.h).
+
+Argument marshalling only: every computation happens in the library (host
+table builder and HIP kernels).  Functions keep the C names; device arrays are
+torch tensors on a ROCm device (their data pointers are passed), host arrays
+are numpy arrays.  A missing library is an ImportError: there is no fallback.
+"""
+import ctypes as C
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "_lib", "libdpc.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"libdpc.so not found at {LIB_PATH}; build it with "
+        "`python -m paper_2107_02103_amd.build` (or __graft_entry__.build())")
+# PyTorch-ROCm ships its own HIP runtime with the same SONAME as the system one
+# (libamdhip64.so.7).  Loading torch first makes the dynamic linker bind
+# libdpc.so to that already-loaded runtime, so that the library, torch's
+# allocator and torch's streams share one HIP runtime in the process.
+try:
+    import torch  # noqa: F401
+except ImportError:  # the C library can be used without torch
+    torch = None
+_lib = C.CDLL(LIB_PATH)
+
+DPC_OK, DPC_EINVAL, DPC_ERANGE, DPC_EHIP, DPC_ENOTSUP = 0, -1, -2, -3, -4
+DPC_F64, DPC_F32, DPC_F32_ACC64 = 0, 1, 2
+DPC_MAX_TYPES, DPC_MAX_M1 = 8, 256
+EXPORTED = ("dpc_strerror", "dpc_last_hip_error", "dpc_version", "dpc_table_layout", "dpc_build_table",
+            "dpc_se_a_tab_fwd", "dpc_se_a_tab_bwd")
+
+
+class dpc_range(C.Structure):
+    _fields_ = [("lo", C.c_double), ("d1", C.c_double), ("d2", C.c_double),
+                ("L1", C.c_int64), ("L2", C.c_int64), ("offset", C.c_int64)]
+
+
+class dpc_net(C.Structure):
+    _fields_ = [("n_layers", C.c_int), ("widths", C.POINTER(C.c_int)),
+                ("W", C.POINTER(C.POINTER(C.c_double))), ("b", C.POINTER(C.POINTER(C.c_double)))]
+
+
+_lib.dpc_strerror.restype = C.c_char_p
+_lib.dpc_strerror.argtypes = [C.c_int]
+_lib.dpc_version.restype = C.c_int
+_lib.dpc_last_hip_error.restype = C.c_char_p
+_lib.dpc_table_layout.restype = C.c_int
+_lib.dpc_table_layout.argtypes = [C.c_int, C.c_int, C.POINTER(dpc_range), C.c_int,
+                                  C.POINTER(C.c_size_t)]
+_lib.dpc_build_table.restype = C.c_int
+_lib.dpc_build_table.argtypes = [C.POINTER(dpc_net), C.POINTER(dpc_range), C.c_int, C.c_void_p]
+_lib.dpc_se_a_tab_fwd.restype = C.c_int
+_lib.dpc_se_a_tab_fwd.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.POINTER(C.c_int),
+                                  C.c_int, C.c_int, C.POINTER(dpc_range), C.c_void_p,
+                                  C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+_lib.dpc_se_a_tab_bwd.restype = C.c_int
+_lib.dpc_se_a_tab_bwd.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.POINTER(C.c_int),
+                                  C.c_int, C.POINTER(dpc_range), C.c_void_p, C.c_void_p,
+                                  C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+
+
+class DpcError(RuntimeError):
+    def __init__(self, status, where=""):
+        self.status = status
+        msg = f"{where}: {dpc_strerror(status)} ({status})"
+        if status == DPC_EHIP:
+            msg += ": " + dpc_last_hip_error()
+        super().__init__(msg)
+
+
+def _check(status, where):
+    if status != DPC_OK:
+        raise DpcError(status, where)
+
+
+def dpc_strerror(status):
+    return _lib.dpc_strerror(int(status)).decode()
+
+
+def dpc_last_hip_error():
+    return _lib.dpc_last_hip_error().decode()
+
+
+def dpc_version():
+    return int(_lib.dpc_version())
+
+
+def make_ranges(lo, d1, L1, d2, L2):
+    """ctypes array of dpc_range from per-pair sequences."""
+    n = len(lo)
+    arr = (dpc_range * n)()
+    for p in range(n):
+        arr[p].lo, arr[p].d1, arr[p].d2 = float(lo[p]), float(d1[p]), float(d2[p])
+        arr[p].L1, arr[p].L2, arr[p].offset = int(L1[p]), int(L2[p]), 0
+    return arr
+
+
+def dpc_table_layout(ranges, m1, dtype):
+    """Fills ranges[p].offset; returns the coefficient buffer size in bytes."""
+    total = C.c_size_t(0)
+    _check(_lib.dpc_table_layout(len(ranges), int(m1), ranges, int(dtype), C.byref(total)),
+           "dpc_table_layout")
+    return int(total.value)
+
+
+def _net_struct(net):
+    W = [np.ascontiguousarray(w, np.float64) for w in net["W"]]
+    b = [np.ascontiguousarray(v, np.float64) for v in net["b"]]
+    widths = [W[0].shape[0]] + [w.shape[1] for w in W]
+    keep = (W, b)
+    s = dpc_net()
+    s.n_layers = len(W)
+    s.widths = (C.c_int * len(widths))(*widths)
+    s.W = (C.POINTER(C.c_double) * len(W))(*[w.ctypes.data_as(C.POINTER(C.c_double)) for w in W])
+    s.b = (C.POINTER(C.c_double) * len(b))(*[v.ctypes.data_as(C.POINTER(C.c_double)) for v in b])
+    return s, keep
+
+
+def dpc_build_table(net, rng, dtype, host_out):
+    """Tabulate one net (dict of W, b lists) over one dpc_range into host_out
+    (a numpy array with room for (L1 + L2) * 6 * m1 coefficients)."""
+    s, keep = _net_struct(net)
+    m1 = keep[0][-1].shape[1]
+    need = (rng.L1 + rng.L2) * 6 * m1
+    want = np.float64 if dtype == DPC_F64 else np.float32
+    if host_out.dtype != want or host_out.size < need or not host_out.flags.c_contiguous:
+        raise ValueError("host_out has the wrong dtype, size or layout")
+    _check(_lib.dpc_build_table(C.byref(s), C.byref(rng), int(dtype),
+                                host_out.ctypes.data_as(C.c_void_p)), "dpc_build_table")
+    return host_out
+
+
+def build_tables(nets, ranges, dtype):
+    """All pairs' tables in one host buffer laid out by dpc_table_layout."""
+    m1 = np.asarray(nets[0]["W"][-1]).shape[1]
+    nbytes = dpc_table_layout(ranges, m1, dtype)
+    want = np.float64 if dtype == DPC_F64 else np.float32
+    buf = np.zeros(nbytes // np.dtype(want).itemsize, want)
+    for p, net in enumerate(nets):
+        r = ranges[p]
+        n = (r.L1 + r.L2) * 6 * m1
+        dpc_build_table(net, r, dtype, buf[r.offset:r.offset + n])
+    return buf
+
+
+def _ptr(x, dtype=None, name="?"):
+    """Device pointer of a contiguous torch tensor (or an int address)."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if not x.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and x.dtype != dtype:
+        raise TypeError(f"{name} has dtype {x.dtype}, expected {dtype}")
+    return x.data_ptr()
+
+
+def _sel(sel):
+    return (C.c_int * len(sel))(*[int(s) for s in sel])
+
+
+def _stream(stream):
+    if stream is None:
+        return None
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def dpc_se_a_tab_fwd(stream, dtype, nloc, ntypes, sel, m1, m2, ranges, coeff, atype, nlist, em,
+                     T, D):
+    _check(_lib.dpc_se_a_tab_fwd(_stream(stream), int(dtype), int(nloc), int(ntypes), _sel(sel),
+                                 int(m1), int(m2), ranges, _ptr(coeff, name="coeff"),
+                                 _ptr(atype, name="atype"), _ptr(nlist, name="nlist"),
+                                 _ptr(em, name="em"), _ptr(T, name="T"), _ptr(D, name="D")),
+           "dpc_se_a_tab_fwd")
+
+
+def dpc_se_a_tab_bwd(stream, dtype, nloc, ntypes, sel, m1, ranges, coeff, atype, nlist, em,
+                     dE_dT, dE_dem):
+    _check(_lib.dpc_se_a_tab_bwd(_stream(stream), int(dtype), int(nloc), int(ntypes), _sel(sel),
+                                 int(m1), ranges, _ptr(coeff, name="coeff"),
+                                 _ptr(atype, name="atype"), _ptr(nlist, name="nlist"),
+                                 _ptr(em, name="em"), _ptr(dE_dT, name="dE_dT"),
+                                 _ptr(dE_dem, name="dE_dem")),
+           "dpc_se_a_tab_bwd")

@@ -1,0 +1,148 @@
+"""C-ABI checks that need no GPU: exported symbols, table layout, the host
+table builder against the oracle (by evaluation) and argument validation."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2107_02103_amd as P
+from paper_2107_02103_amd import binding as B
+from oracle.table import build_table as oracle_table
+from synth import make_inputs
+from synth.configs import get_config
+from synth.system import random_net
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "dpc.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(dpc_\w+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = _declared()
+    assert set(names) == set(B.EXPORTED)
+    lib = C.CDLL(B.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_strerror_and_version():
+    assert P.dpc_version() >= 100
+    for s in (0, -1, -2, -3, -4):
+        assert len(P.dpc_strerror(s)) > 1
+    assert P.dpc_strerror(-99) == "unknown status"
+
+
+def test_table_layout_offsets():
+    r = P.make_ranges([0.0, -1.0], [0.01, 0.02], [10, 20], [0.1, 0.1], [2, 3], )
+    nbytes = P.dpc_table_layout(r, 7, P.DPC_F64)
+    assert r[0].offset == 0 and r[1].offset == 12 * 6 * 7
+    assert nbytes == (12 + 23) * 6 * 7 * 8
+    assert P.dpc_table_layout(r, 7, P.DPC_F32) == nbytes // 2
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(d1=0.0), B.DPC_ERANGE), (dict(d2=-0.1), B.DPC_ERANGE), (dict(L1=0), B.DPC_ERANGE),
+    (dict(L2=0), B.DPC_ERANGE), (dict(lo=float("nan")), B.DPC_ERANGE)])
+def test_table_layout_rejects_bad_ranges(bad, code):
+    kw = dict(lo=0.0, d1=0.01, L1=5, d2=0.1, L2=1)
+    kw.update(bad)
+    r = P.make_ranges([kw["lo"]], [kw["d1"]], [kw["L1"]], [kw["d2"]], [kw["L2"]])
+    with pytest.raises(P.DpcError) as e:
+        P.dpc_table_layout(r, 4, P.DPC_F64)
+    assert e.value.status == code
+
+
+def test_table_layout_rejects_bad_sizes():
+    r = P.make_ranges([0.0], [0.01], [5], [0.1], [1])
+    for m1, dt, code in ((0, 0, B.DPC_EINVAL), (257, 0, B.DPC_ENOTSUP), (4, 7, B.DPC_EINVAL)):
+        with pytest.raises(P.DpcError) as e:
+            P.dpc_table_layout(r, m1, dt)
+        assert e.value.status == code
+
+
+def _eval_lib(buf, rng, m1, x):
+    """Value/slope/curvature of the library's table at x (test-side Horner)."""
+    L1, L2 = rng.L1, rng.L2
+    c = buf[rng.offset:rng.offset + (L1 + L2) * 6 * m1].reshape(L1 + L2, 6, m1).astype(np.float64)
+    x_up = rng.lo + L1 * rng.d1
+    l = np.where(x < x_up, np.clip(np.floor((x - rng.lo) / rng.d1), 0, L1 - 1),
+                 L1 + np.clip(np.floor((x - x_up) / rng.d2), 0, L2 - 1)).astype(int)
+    t = np.where(l < L1, x - (rng.lo + l * rng.d1), x - (x_up + (l - L1) * rng.d2))[:, None]
+    q = c[l]                                      # [n, 6, m1]
+    g = sum(q[:, k] * t ** k for k in range(6))
+    g1 = sum(k * q[:, k] * t ** (k - 1) for k in range(1, 6))
+    g2 = sum(k * (k - 1) * q[:, k] * t ** (k - 2) for k in range(2, 6))
+    return g, g1, g2
+
+
+@pytest.mark.parametrize("seed,widths", [(0, (1, 25, 50, 100)), (1, (1, 4, 8, 16)), (2, (1, 3, 6, 6))])
+def test_build_table_matches_oracle_by_evaluation(seed, widths):
+    net = random_net(np.random.default_rng(seed), widths)
+    lo, d1, L1, d2, L2 = -0.7, 0.01, 450, 0.1, 45
+    r = P.make_ranges([lo], [d1], [L1], [d2], [L2])
+    buf = P.build_tables([net], r, P.DPC_F64)
+    ot = oracle_table(net, lo, d1, L1, d2, L2)
+    x = np.random.default_rng(seed).uniform(lo, ot.x_end - 1e-9, 5000)
+    g, g1, g2 = _eval_lib(buf, r[0], widths[-1], x)
+    o, o1, o2 = ot.evaluate(x, order=2)
+    s = np.max(np.abs(o))
+    assert np.max(np.abs(g - o)) <= 1e-13 * s
+    assert np.max(np.abs(g1 - o1)) <= 1e-9 * np.max(np.abs(o1))
+    assert np.max(np.abs(g2 - o2)) <= 1e-5 * np.max(np.abs(o2))
+
+
+def test_build_table_f32_is_rounded_f64():
+    net = random_net(np.random.default_rng(3), (1, 25, 50, 100))
+    r = P.make_ranges([-0.5], [0.01], [100], [0.1], [10])
+    b64 = P.build_tables([net], r, P.DPC_F64)
+    r32 = P.make_ranges([-0.5], [0.01], [100], [0.1], [10])
+    b32 = P.build_tables([net], r32, P.DPC_F32)
+    np.testing.assert_array_equal(b32, b64.astype(np.float32))
+
+
+def test_build_table_rejects_bad_nets():
+    net = random_net(np.random.default_rng(3), (1, 4, 8))
+    r = P.make_ranges([-0.5], [0.01], [10], [0.1], [1])
+    out = np.zeros((11 * 6 * 8,))
+    bad = {"W": [np.zeros((2, 4)), net["W"][1]], "b": net["b"]}     # widths[0] != 1
+    with pytest.raises(P.DpcError) as e:
+        P.dpc_build_table(bad, r[0], P.DPC_F64, out)
+    assert e.value.status == B.DPC_EINVAL
+    with pytest.raises(ValueError):                                   # output too small
+        P.dpc_build_table(net, r[0], P.DPC_F64, np.zeros(10))
+
+
+def test_kernel_entry_points_validate_before_launch():
+    # every call below must fail (or no-op) on the host without touching HIP
+    sel = [4, 4]
+    r = P.make_ranges([0.0] * 4, [0.01] * 4, [5] * 4, [0.1] * 4, [1] * 4)
+    P.dpc_table_layout(r, 8, P.DPC_F64)
+    fake = 4096  # never dereferenced: validation fails first
+    cases = [
+        (dict(dtype=9), B.DPC_EINVAL), (dict(m2=9), B.DPC_EINVAL), (dict(m2=0), B.DPC_EINVAL),
+        (dict(ntypes=9, sel=[1] * 9), B.DPC_ENOTSUP), (dict(m1=300, m2=4), B.DPC_ENOTSUP),
+        (dict(nloc=-1), B.DPC_EINVAL), (dict(sel=[4, -1]), B.DPC_EINVAL),
+        (dict(em=0), B.DPC_EINVAL), (dict(T=0), B.DPC_EINVAL),
+    ]
+    for kw, code in cases:
+        a = dict(stream=0, dtype=P.DPC_F64, nloc=3, ntypes=2, sel=sel, m1=8, m2=4, ranges=r,
+                 coeff=fake, atype=fake, nlist=fake, em=fake, T=fake, D=fake)
+        a.update(kw)
+        if "ntypes" in kw:
+            a["ranges"] = P.make_ranges([0.0] * 81, [0.01] * 81, [5] * 81, [0.1] * 81, [1] * 81)
+        with pytest.raises(P.DpcError) as e:
+            P.dpc_se_a_tab_fwd(**a)
+        assert e.value.status == code, kw
+    bad = P.make_ranges([0.0] * 4, [0.01] * 4, [5] * 4, [0.0] * 4, [1] * 4)
+    with pytest.raises(P.DpcError) as e:
+        P.dpc_se_a_tab_bwd(0, P.DPC_F64, 3, 2, sel, 8, bad, fake, fake, fake, fake, fake, fake)
+    assert e.value.status == B.DPC_ERANGE
+    # nloc = 0 is a no-op that launches nothing
+    P.dpc_se_a_tab_fwd(0, P.DPC_F64, 0, 2, sel, 8, 4, r, 0, 0, 0, 0, 0, 0)
+    P.dpc_se_a_tab_bwd(0, P.DPC_F64, 0, 2, sel, 8, r, 0, 0, 0, 0, 0, 0)

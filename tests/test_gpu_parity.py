@@ -1,0 +1,196 @@
+"""GPU parity: the HIP kernels (through the C ABI) against the oracle on the
+same seeded inputs.  fp64 to 1e-12 and fp32 / mixed modes to 1e-5, per-atom
+normwise and abs-sum-scaled componentwise."""
+import numpy as np
+import pytest
+
+from synth import make_inputs
+from synth.configs import get_config
+
+from parity import TOL, compare, oracle_abs_bounds, oracle_fwd_bwd
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+_CACHE = {}
+
+
+def _inputs(key):
+    if key not in _CACHE:
+        _CACHE.clear()          # keep at most one big config resident
+        print(f"[gpu-parity] generating {key}", flush=True)
+        _CACHE[key] = make_inputs(get_config(key))
+    return _CACHE[key]
+
+
+def _mode(dtype):
+    import paper_2107_02103_amd as P
+    return {"f64": (P.DPC_F64, np.float64), "f32": (P.DPC_F32, np.float32),
+            "f32acc64": (P.DPC_F32_ACC64, np.float32)}[dtype]
+
+
+def _run_gpu(x, dtype="f64"):
+    import paper_2107_02103_amd as P
+    mode, store = _mode(dtype)
+    c = x.cfg
+    op = P.SeATab(x.nets, x.lo, x.L1, x.L2, c.d1, c.d2, c.sel, c.m2, dtype=mode)
+    dev = "cuda"
+    em = torch.from_numpy(x.em.astype(store, copy=False)).to(dev)
+    nl = torch.from_numpy(x.nlist).to(dev)
+    at = torch.from_numpy(x.atype).to(dev)
+    dT = torch.from_numpy(x.dT.astype(store, copy=False)).to(dev)
+    T, D = op.forward(em, nl, at)
+    dR = op.backward(em, nl, at, dT)
+    torch.cuda.synchronize()
+    return op, (em, nl, at, dT), (T, D, dR)
+
+
+def _check(x, atoms, got, dtype, with_bounds=True):
+    tol = TOL[dtype]
+    ref = oracle_fwd_bwd(x, atoms, dtype)
+    bounds = oracle_abs_bounds(x, atoms, dtype) if with_bounds else None
+    g = tuple(a[atoms] for a in got)
+    rep = compare(g, ref, bounds, tol)
+    print(f"[gpu-parity] {x.cfg.name} {dtype} atoms={len(atoms)} {rep}", flush=True)
+    assert rep["ok"], rep
+    # padding rows of dE/dR~ are exactly zero
+    assert np.all(g[2][x.nlist[atoms] < 0] == 0)
+
+
+def _sample(n, k, seed=0):
+    rng = np.random.default_rng(seed)
+    s = rng.choice(n, size=min(k, n), replace=False)
+    return np.unique(np.concatenate([s, [0, n - 1]]))
+
+
+@pytest.mark.parametrize("key", ["tiny_fcc", "tiny_alloy", "tiny_water", 0, 1, 2])
+def test_parity_f64(key):
+    x = _inputs(key)
+    _, _, out = _run_gpu(x, "f64")
+    got = tuple(t.cpu().numpy() for t in out)
+    n = x.nlist.shape[0]
+    # every atom normwise against the C oracle, a sample componentwise
+    ref = oracle_fwd_bwd(x, np.arange(n), "f64")
+    rep = compare(got, ref, None, TOL["f64"])
+    print(f"[gpu-parity] {x.cfg.name} all atoms {rep}", flush=True)
+    assert rep["ok"], rep
+    _check(x, _sample(n, 300), got, "f64")
+
+
+@pytest.mark.timeout(600)
+def test_parity_f64_full_size_cu1m():
+    # the benchmarked workload (1,048,576 atoms, sel 512), sampled outputs
+    x = _inputs(3)
+    _, _, out = _run_gpu(x, "f64")
+    atoms = _sample(x.nlist.shape[0], 400, seed=3)
+    got = tuple(t[torch.from_numpy(atoms).cuda()].cpu().numpy() for t in out)
+    tol = TOL["f64"]
+    ref = oracle_fwd_bwd(x, atoms, "f64")
+    bounds = oracle_abs_bounds(x, atoms, "f64")
+    rep = compare(got, ref, bounds, tol)
+    print(f"[gpu-parity] cu1m sampled {rep}", flush=True)
+    assert rep["ok"], rep
+    del out
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("dtype", ["f32", "f32acc64", "f64"])
+def test_parity_water_large_modes(dtype):
+    x = _inputs(4)
+    _, _, out = _run_gpu(x, dtype)
+    atoms = _sample(x.nlist.shape[0], 300, seed=4)
+    got = tuple(t[torch.from_numpy(atoms).cuda()].cpu().numpy().astype(np.float64) for t in out)
+    tol = TOL[dtype]
+    rep = compare(got, oracle_fwd_bwd(x, atoms, dtype), oracle_abs_bounds(x, atoms, dtype), tol)
+    print(f"[gpu-parity] water110592 {dtype} sampled {rep}", flush=True)
+    assert rep["ok"], rep
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f32acc64"])
+def test_parity_small_fp32_modes(dtype):
+    x = _inputs(1)
+    _, _, out = _run_gpu(x, dtype)
+    got = tuple(t.cpu().numpy().astype(np.float64) for t in out)
+    _check(x, _sample(x.nlist.shape[0], 300, seed=1), got, dtype)
+
+
+def test_deterministic_bitwise():
+    x = _inputs(2)
+    op, (em, nl, at, dT), out1 = _run_gpu(x, "f64")
+    T2, D2 = op.forward(em, nl, at)
+    dR2 = op.backward(em, nl, at, dT)
+    torch.cuda.synchronize()
+    assert torch.equal(out1[0], T2) and torch.equal(out1[1], D2) and torch.equal(out1[2], dR2)
+
+
+def _synthetic(nloc, sel, m1, m2, seed, lo=-0.6, L1=300, L2=30, d1=0.01, d2=0.1):
+    """Inputs with hand-placed neighbours for edge cases (oracle-ready)."""
+    from synth.system import Inputs, random_net
+    from synth.configs import Config
+    rng = np.random.default_rng(seed)
+    nt = len(sel)
+    cfg = Config("edge", "fcc", 1, rc=1.0, rcs=0.5, sel=tuple(sel), widths=(1, 8, 16, m1),
+                 m2=m2, d1=d1, d2=d2)
+    nnei = sum(sel)
+    nlist = np.full((nloc, nnei), -1, np.int32)
+    em = np.zeros((nloc, nnei, 4))
+    x_up = lo + L1 * d1
+    x_end = x_up + L2 * d2
+    for i in range(nloc):
+        k = rng.integers(0, nnei + 1)
+        slots = rng.choice(nnei, size=k, replace=False)
+        nlist[i, slots] = rng.integers(0, nloc, size=k)
+        # slightly below lo (interval 0 extrapolated by less than a fifth of a
+        # step, where the quintic is still well conditioned), inside the range,
+        # in the band and past its end (clamped)
+        em[i, slots, 0] = rng.uniform(lo - 0.2 * d1, x_end + 0.5, size=k)
+        em[i, slots, 1:] = rng.normal(size=(k, 3))
+    atype = rng.integers(0, nt, size=nloc).astype(np.int32)
+    nets = [random_net(rng, cfg.widths) for _ in range(nt * nt)]
+    npair = nt * nt
+    return Inputs(cfg=cfg, atype=atype, nlist=nlist, em=em, nets=nets, lo=np.full(npair, lo),
+                  L1=np.full(npair, L1), L2=np.full(npair, L2), s_hat_max=np.zeros(npair),
+                  stats={}, dT=rng.normal(size=(nloc, m1, 4)), n_valid=int((nlist >= 0).sum()))
+
+
+@pytest.mark.parametrize("sel,m1,m2", [((3, 70), 100, 16), ((64,), 64, 64), ((5, 1, 60), 200, 7),
+                                       ((130,), 1, 1), ((1,), 100, 100)])
+def test_edge_shapes_and_ranges(sel, m1, m2):
+    # ragged nnei, m1 not a multiple of 64 (and m1 > 128), m2 = m1, a single
+    # channel, inputs below lo and beyond the band (clamped), empty atoms
+    x = _synthetic(37, sel, m1, m2, seed=sum(sel) + m1)
+    x.nlist[5] = -1
+    x.em[5] = 0
+    _, _, out = _run_gpu(x, "f64")
+    got = tuple(t.cpu().numpy() for t in out)
+    _check(x, np.arange(37), got, "f64")
+    assert np.all(got[0][5] == 0) and np.all(got[1][5] == 0) and np.all(got[2][5] == 0)
+
+
+def test_empty_and_single_atom():
+    import paper_2107_02103_amd as P
+    x = _synthetic(1, (40,), 100, 16, seed=3)
+    _, _, out = _run_gpu(x, "f64")
+    _check(x, np.arange(1), tuple(t.cpu().numpy() for t in out), "f64")
+    c = x.cfg
+    op = P.SeATab(x.nets, x.lo, x.L1, x.L2, c.d1, c.d2, c.sel, c.m2)
+    e = torch.zeros((0, 40, 4), dtype=torch.float64, device="cuda")
+    nl = torch.zeros((0, 40), dtype=torch.int32, device="cuda")
+    at = torch.zeros((0,), dtype=torch.int32, device="cuda")
+    T, D = op.forward(e, nl, at)
+    dR = op.backward(e, nl, at, torch.zeros((0, 100, 4), dtype=torch.float64, device="cuda"))
+    torch.cuda.synchronize()
+    assert T.shape == (0, 100, 4) and D.shape == (0, 100, 16) and dR.shape == (0, 40, 4)
+
+
+def test_nan_stays_in_its_atom():
+    x = _synthetic(9, (50,), 100, 16, seed=4)
+    j = int(np.nonzero(x.nlist[2] >= 0)[0][0])
+    x.em[2, j, 1] = np.nan
+    _, _, out = _run_gpu(x, "f64")
+    T, D, dR = (t.cpu().numpy() for t in out)
+    assert np.isnan(T[2]).any()
+    others = [i for i in range(9) if i != 2]
+    assert np.isfinite(T[others]).all() and np.isfinite(D[others]).all() and np.isfinite(dR[others]).all()
+    _check(x, np.array(others), (T, D, dR), "f64", with_bounds=False)
