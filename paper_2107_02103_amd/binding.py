@@ -89,6 +89,11 @@ def dpc_version():
     return int(_lib.dpc_version())
 
 
+def table_ld(m1):
+    """Row stride of the coefficient table (DPC_TABLE_LD in dpc.h)."""
+    return (int(m1) + 3) // 4 * 4
+
+
 def make_ranges(lo, d1, L1, d2, L2):
     """ctypes array of dpc_range from per-pair sequences."""
     n = len(lo)
@@ -122,10 +127,10 @@ def _net_struct(net):
 
 def dpc_build_table(net, rng, dtype, host_out):
     """Tabulate one net (dict of W, b lists) over one dpc_range into host_out
-    (a numpy array with room for (L1 + L2) * 6 * m1 coefficients)."""
+    (a numpy array with room for (L1 + L2) * 6 * table_ld(m1) coefficients)."""
     s, keep = _net_struct(net)
     m1 = keep[0][-1].shape[1]
-    need = (rng.L1 + rng.L2) * 6 * m1
+    need = (rng.L1 + rng.L2) * 6 * table_ld(m1)
     want = np.float64 if dtype == DPC_F64 else np.float32
     if host_out.dtype != want or host_out.size < need or not host_out.flags.c_contiguous:
         raise ValueError("host_out has the wrong dtype, size or layout")
@@ -142,7 +147,7 @@ def build_tables(nets, ranges, dtype):
     buf = np.zeros(nbytes // np.dtype(want).itemsize, want)
     for p, net in enumerate(nets):
         r = ranges[p]
-        n = (r.L1 + r.L2) * 6 * m1
+        n = (r.L1 + r.L2) * 6 * table_ld(m1)
         dpc_build_table(net, r, dtype, buf[r.offset:r.offset + n])
     return buf
 

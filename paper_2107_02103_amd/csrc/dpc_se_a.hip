@@ -5,19 +5,21 @@
 // evaluated only over valid neighbours; D = T (T<)^T.  The backward kernel
 // maps dE/dT to dE/dR~ through the polynomial and its derivative.
 //
-// Forward mapping: one wavefront per atom, lanes = channels (channel m is
-// handled by lane m % 64).  The neighbour list is scanned 64 slots at a time:
-// each lane locates the interval of its slot, a ballot gives the valid slots,
-// and the wave then walks the valid slots in order with the slot's row of R~
-// and its interval offset uniform across the wave.  Coefficients of the
-// current interval stay in registers until the interval changes (neighbours
-// are distance-sorted, so consecutive slots often share an interval).
+// Both kernels: one wavefront per atom, lanes = channels.  Lane l owns the
+// CPL consecutive channels CPL*l .. CPL*l + CPL - 1, so that one 16-byte load
+// brings the coefficient of t^q for all of them (table rows are padded to a
+// multiple of 4 channels).  The neighbour list is first compacted, 64 slots
+// at a time, into per-wave records {t, interval offset, slot} in LDS; the wave
+// then walks the records with the record, the R~ row (scalar loads) and the
+// interval uniform across the wave.  The coefficients of the current interval
+// stay in registers until the interval changes: neighbours are distance
+// sorted, so consecutive records often share an interval.
 //
-// Backward mapping: one wavefront per atom, lanes = neighbour slots, a loop
-// over the channels with dE/dT_i[m][:] uniform across the wave.  Each lane
-// keeps v_k = sum_m dT[m][k] g_m and u_k = sum_m dT[m][k] g'_m, then
-// dE/dR~[k] = v_k + (k == 0) sum_k' u_k' R~[k'], which regroups
-// sum_m g'_m sum_k' dT[m][k'] R~[k'] without changing its value.
+// Forward: acc[k] += g_m(t) * R~[k] per channel, then T and D = T (T<)^T.
+// Backward: for every record each lane forms its share of
+//   dE/dR~[k] = sum_m dT[m][k] g_m + (k == 0) sum_m g'_m sum_k' dT[m][k'] R~[k']
+// over its channels; the shares of a batch of records are summed across
+// lanes through LDS (a transpose: each lane adds up a strip of the batch).
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -27,20 +29,29 @@
 
 namespace {
 
-constexpr int kWaves = 4;  // wavefronts per workgroup
+constexpr int kWaves = 4;      // wavefronts per workgroup (one atom each)
+constexpr int kSeg = 128;      // neighbour slots compacted per segment
+constexpr int kBatch = 8;      // records per cross-lane reduction in the backward pass
 
-struct PairRange {          // one ordered type pair's table, as the kernels see it
+struct PairRange {             // one ordered type pair's table, as the kernels see it
   double lo, d1, d2;
   int L1, L2;
-  int offset;               // element offset of the pair's coefficients
+  int offset;                  // element offset of the pair's coefficients
   int pad;
 };
 
 struct Geo {
-  int nloc, nnei, ntypes, m1, m2;
-  int blk_end[DPC_MAX_TYPES];   // slot index one past the end of each sel block
+  int nloc, nnei, ntypes, m1, m2, ld;
+  int blk_end[DPC_MAX_TYPES];  // slot index one past the end of each sel block
   PairRange pr[DPC_MAX_TYPES * DPC_MAX_TYPES];
 };
+
+struct Rec {                   // one valid neighbour, as staged in LDS
+  double t;                    // offset from the left node of its interval
+  int off;                     // element offset of the interval's coefficient rows
+  int slot;                    // neighbour slot; bit 30 set = beyond the table (clamped)
+};
+constexpr int kClamped = 1 << 30;
 
 __device__ __forceinline__ int block_of(const Geo& g, int j) {
   int b = 0;
@@ -78,9 +89,51 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <typename TA, typename TI>
-__device__ __forceinline__ TA fma_acc(TI a, TI b, TA c) {
-  return fma((TA)a, (TA)b, c);
+__device__ __forceinline__ int lanes_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
+}
+
+// Compact the valid slots [s0, s1) of atom i into records; returns their count.
+// Invalid slots get a zero row in `zero_out` when it is non-null.
+template <typename TI, typename TA>
+__device__ __forceinline__ int compact(const Geo& g, int ai, const int* nli, const TI* emi,
+                                       int s0, int s1, Rec* rec, TA* zero_out, int lane) {
+  int n = 0;
+  for (int base = s0; base < s1; base += 64) {
+    const int j = base + lane;
+    bool valid = false;
+    Rec r;
+    if (j < s1) {
+      valid = nli[j] >= 0;
+      if (valid) {
+        const PairRange& P = g.pr[ai * g.ntypes + block_of(g, j)];
+        int l;
+        bool cl;
+        locate(P, (double)emi[(size_t)j * 4], l, r.t, cl);
+        r.off = P.offset + l * 6 * g.ld;
+        r.slot = j | (cl ? kClamped : 0);
+      } else if (zero_out) {
+        TA* o = zero_out + (size_t)j * 4;
+        o[0] = o[1] = o[2] = o[3] = (TA)0;
+      }
+    }
+    const uint64_t mask = __ballot(valid);
+    if (valid) rec[n + lanes_below(mask)] = r;
+    n += __popcll(mask);
+  }
+  return n;
+}
+
+// Coefficients of t^q (q = 0..5) for the lane's CPL channels of one interval.
+template <typename TI, int CPL>
+__device__ __forceinline__ void load_coef(const TI* __restrict__ rows, int ld, int c0,
+                                          TI (&cf)[6][CPL]) {
+#pragma unroll
+  for (int q = 0; q < 6; ++q) {
+#pragma unroll
+    for (int h = 0; h < CPL; ++h) cf[q][h] = rows[q * ld + c0 + h];
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -96,12 +149,9 @@ __global__ __launch_bounds__(64 * kWaves) void se_a_fwd_kernel(
   const int wave = threadIdx.x >> 6;
   const int i = __builtin_amdgcn_readfirstlane(blockIdx.x * kWaves + wave);
   if (i >= g.nloc) return;
-  const int nnei = g.nnei, m1 = g.m1, m2 = g.m2;
-  TA* sT = reinterpret_cast<TA*>(smem) + wave * m2 * 4;                       // [m2][4]
-  TI* st = reinterpret_cast<TI*>(reinterpret_cast<TA*>(smem) + kWaves * m2 * 4) + wave * 64;
-  int* so = reinterpret_cast<int*>(reinterpret_cast<TI*>(reinterpret_cast<TA*>(smem) +
-                                                          kWaves * m2 * 4) + kWaves * 64) +
-            wave * 64;
+  const int nnei = g.nnei, m1 = g.m1, m2 = g.m2, ld = g.ld;
+  Rec* rec = reinterpret_cast<Rec*>(smem) + wave * kSeg;
+  TA* sT = reinterpret_cast<TA*>(reinterpret_cast<Rec*>(smem) + kWaves * kSeg) + wave * m2 * 4;
 
   const int ai = __builtin_amdgcn_readfirstlane(atype[i]);
   if (ai < 0 || ai >= g.ntypes) {  // invalid type: the atom's outputs become NaN
@@ -112,65 +162,49 @@ __global__ __launch_bounds__(64 * kWaves) void se_a_fwd_kernel(
   }
   const TI* emi = em + (size_t)i * nnei * 4;
   const int* nli = nlist + (size_t)i * nnei;
+  const int c0 = min(lane * CPL, ld - CPL);   // lanes past the last channel reload a valid row
 
   TA acc[CPL][4];
-  TI c[CPL][6];
+  TI cf[6][CPL];
 #pragma unroll
   for (int h = 0; h < CPL; ++h) {
 #pragma unroll
     for (int k = 0; k < 4; ++k) acc[h][k] = (TA)0;
+  }
 #pragma unroll
-    for (int q = 0; q < 6; ++q) c[h][q] = (TI)0;
+  for (int q = 0; q < 6; ++q) {
+#pragma unroll
+    for (int h = 0; h < CPL; ++h) cf[q][h] = (TI)0;
   }
   int cur = -1;
 
-  for (int base = 0; base < nnei; base += 64) {
-    const int j = base + lane;
-    bool valid = false;
-    TI tt = (TI)0;
-    int off = 0;
-    if (j < nnei && nli[j] >= 0) {
-      const PairRange& P = g.pr[ai * g.ntypes + block_of(g, j)];
-      int l;
-      double t;
-      bool cl;
-      locate(P, (double)emi[(size_t)j * 4], l, t, cl);
-      off = P.offset + l * 6 * m1;
-      tt = (TI)t;
-      valid = true;
-    }
-    uint64_t mask = __ballot(valid);
-    st[lane] = tt;
-    so[lane] = off;
+  for (int s0 = 0; s0 < nnei; s0 += kSeg) {
+    const int n = compact<TI, TA>(g, ai, nli, emi, s0, min(nnei, s0 + kSeg), rec, nullptr, lane);
     wave_sync();
-    while (mask) {
-      const int jj = __builtin_ctzll(mask);
-      mask &= mask - 1;
-      const TI t = st[jj];
-      const int o = __builtin_amdgcn_readfirstlane(so[jj]);
-      const TI* r = emi + (size_t)(base + jj) * 4;
-      const TI r0 = r[0], r1 = r[1], r2 = r[2], r3 = r[3];
-      if (o != cur) {
-        cur = o;
-#pragma unroll
-        for (int h = 0; h < CPL; ++h) {
-          const int m = lane + 64 * h;
-#pragma unroll
-          for (int q = 0; q < 6; ++q) c[h][q] = (m < m1) ? coeff[o + q * m1 + m] : (TI)0;
-        }
+    for (int e = 0; e < n; ++e) {
+      const Rec r = rec[e];
+      const int off = __builtin_amdgcn_readfirstlane(r.off);
+      const int slot = __builtin_amdgcn_readfirstlane(r.slot) & (kClamped - 1);
+      const TI* R = emi + (size_t)slot * 4;
+      const TI r0 = R[0], r1 = R[1], r2 = R[2], r3 = R[3];
+      if (off != cur) {
+        cur = off;
+        load_coef<TI, CPL>(coeff + off, ld, c0, cf);
       }
+      const TI t = (TI)r.t;
 #pragma unroll
       for (int h = 0; h < CPL; ++h) {
-        TI gv = c[h][5];
-        gv = fma(gv, t, c[h][4]);
-        gv = fma(gv, t, c[h][3]);
-        gv = fma(gv, t, c[h][2]);
-        gv = fma(gv, t, c[h][1]);
-        gv = fma(gv, t, c[h][0]);
-        acc[h][0] = fma_acc<TA>(gv, r0, acc[h][0]);
-        acc[h][1] = fma_acc<TA>(gv, r1, acc[h][1]);
-        acc[h][2] = fma_acc<TA>(gv, r2, acc[h][2]);
-        acc[h][3] = fma_acc<TA>(gv, r3, acc[h][3]);
+        TI gv = cf[5][h];
+        gv = fma(gv, t, cf[4][h]);
+        gv = fma(gv, t, cf[3][h]);
+        gv = fma(gv, t, cf[2][h]);
+        gv = fma(gv, t, cf[1][h]);
+        gv = fma(gv, t, cf[0][h]);
+        const TA ga = (TA)gv;
+        acc[h][0] = fma(ga, (TA)r0, acc[h][0]);
+        acc[h][1] = fma(ga, (TA)r1, acc[h][1]);
+        acc[h][2] = fma(ga, (TA)r2, acc[h][2]);
+        acc[h][3] = fma(ga, (TA)r3, acc[h][3]);
       }
     }
     wave_sync();
@@ -179,7 +213,7 @@ __global__ __launch_bounds__(64 * kWaves) void se_a_fwd_kernel(
   // T rows and the first m2 rows for D
 #pragma unroll
   for (int h = 0; h < CPL; ++h) {
-    const int m = lane + 64 * h;
+    const int m = lane * CPL + h;
     if (m < m1) {
       TA* Tm = T + ((size_t)i * m1 + m) * 4;
 #pragma unroll
@@ -193,7 +227,7 @@ __global__ __launch_bounds__(64 * kWaves) void se_a_fwd_kernel(
   wave_sync();
 #pragma unroll
   for (int h = 0; h < CPL; ++h) {
-    const int m = lane + 64 * h;
+    const int m = lane * CPL + h;
     if (m < m1) {
       TA* Dm = D + ((size_t)i * m1 + m) * m2;
       for (int n = 0; n < m2; ++n) {
@@ -210,16 +244,51 @@ __global__ __launch_bounds__(64 * kWaves) void se_a_fwd_kernel(
 // ---------------------------------------------------------------------------
 // backward: dE/dR~
 // ---------------------------------------------------------------------------
-template <typename TI, typename TA>
+// Sum over lanes of the per-lane shares of a batch of nb <= kBatch records:
+// red[b][lane][k] holds lane `lane`'s share of dE/dR~[k] for record b (only
+// the nl lanes that own channels).  Lane L adds up, for record b = L / 8 and
+// the component pair kk = (L / 4) % 2, every fourth owning lane starting at
+// L % 4; four lanes then combine their sums.
+template <typename TA>
+__device__ __forceinline__ void reduce_batch(const TA* red, int nl, int nb, const Rec* rec,
+                                             TA* dRi, int lane) {
+  const int b = lane >> 3, kk = (lane >> 2) & 1, x = lane & 3;
+  TA s0 = 0, s1 = 0;
+  if (b < nb) {
+    const TA* base = red + (size_t)b * nl * 4 + 2 * kk;
+    for (int l2 = x; l2 < nl; l2 += 4) {
+      s0 += base[l2 * 4];
+      s1 += base[l2 * 4 + 1];
+    }
+  }
+  s0 += __shfl_xor(s0, 1);
+  s1 += __shfl_xor(s1, 1);
+  s0 += __shfl_xor(s0, 2);
+  s1 += __shfl_xor(s1, 2);
+  if (b < nb && x == 0) {
+    const int slot = rec[b].slot & (kClamped - 1);
+    TA* o = dRi + (size_t)slot * 4 + 2 * kk;
+    o[0] = s0;
+    o[1] = s1;
+  }
+}
+
+template <typename TI, typename TA, int CPL>
 __global__ __launch_bounds__(64 * kWaves) void se_a_bwd_kernel(
     const Geo g, const TI* __restrict__ coeff, const int* __restrict__ atype,
     const int* __restrict__ nlist, const TI* __restrict__ em, const TI* __restrict__ dT,
     TA* __restrict__ dR) {
+  extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int i = __builtin_amdgcn_readfirstlane(blockIdx.x * kWaves + wave);
   if (i >= g.nloc) return;
-  const int nnei = g.nnei, m1 = g.m1;
+  const int nnei = g.nnei, m1 = g.m1, ld = g.ld;
+  const int nl = (m1 + CPL - 1) / CPL;          // lanes that own channels
+  Rec* rec = reinterpret_cast<Rec*>(smem) + wave * kSeg;
+  TA* red = reinterpret_cast<TA*>(reinterpret_cast<Rec*>(smem) + kWaves * kSeg) +
+            (size_t)wave * kBatch * nl * 4;
+
   const int ai = __builtin_amdgcn_readfirstlane(atype[i]);
   TA* dRi = dR + (size_t)i * nnei * 4;
   if (ai < 0 || ai >= g.ntypes) {  // invalid type: the atom's outputs become NaN
@@ -228,62 +297,83 @@ __global__ __launch_bounds__(64 * kWaves) void se_a_bwd_kernel(
   }
   const TI* emi = em + (size_t)i * nnei * 4;
   const int* nli = nlist + (size_t)i * nnei;
-  const TI* dTi = dT + (size_t)i * m1 * 4;
+  const int c0 = min(lane * CPL, ld - CPL);
+  const bool owner = lane < nl;
 
-  for (int base = 0; base < nnei; base += 64) {
-    const int j = base + lane;
-    TA o0 = 0, o1 = 0, o2 = 0, o3 = 0;
-    if (j < nnei && nli[j] >= 0) {
-      const TI r0 = emi[(size_t)j * 4 + 0], r1 = emi[(size_t)j * 4 + 1];
-      const TI r2 = emi[(size_t)j * 4 + 2], r3 = emi[(size_t)j * 4 + 3];
-      const PairRange& P = g.pr[ai * g.ntypes + block_of(g, j)];
-      int l;
-      double td;
-      bool cl;
-      locate(P, (double)r0, l, td, cl);
-      const TI t = (TI)td;
-      const TI* c = coeff + P.offset + l * 6 * m1;
-      TA v0 = 0, v1 = 0, v2 = 0, v3 = 0, u0 = 0, u1 = 0, u2 = 0, u3 = 0;
-      for (int m = 0; m < m1; ++m) {
-        const TI c0 = c[m], c1 = c[m1 + m], c2 = c[2 * m1 + m];
-        const TI c3 = c[3 * m1 + m], c4 = c[4 * m1 + m], c5 = c[5 * m1 + m];
-        // value and derivative of the quintic by a joint Horner scheme
-        TI p = c5, d = c5;
-        p = fma(p, t, c4);
-        d = fma(d, t, p);
-        p = fma(p, t, c3);
-        d = fma(d, t, p);
-        p = fma(p, t, c2);
-        d = fma(d, t, p);
-        p = fma(p, t, c1);
-        d = fma(d, t, p);
-        p = fma(p, t, c0);
-        const TI* dm = dTi + m * 4;
-        const TI a0 = dm[0], a1 = dm[1], a2 = dm[2], a3 = dm[3];
-        v0 = fma_acc<TA>(a0, p, v0);
-        v1 = fma_acc<TA>(a1, p, v1);
-        v2 = fma_acc<TA>(a2, p, v2);
-        v3 = fma_acc<TA>(a3, p, v3);
-        u0 = fma_acc<TA>(a0, d, u0);
-        u1 = fma_acc<TA>(a1, d, u1);
-        u2 = fma_acc<TA>(a2, d, u2);
-        u3 = fma_acc<TA>(a3, d, u3);
+  // dE/dT of the lane's channels (zero for lanes past the last channel)
+  TA dt[CPL][4];
+#pragma unroll
+  for (int h = 0; h < CPL; ++h) {
+    const int m = lane * CPL + h;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) dt[h][k] = (m < m1) ? (TA)dT[((size_t)i * m1 + m) * 4 + k] : (TA)0;
+  }
+  TI cf[6][CPL];
+#pragma unroll
+  for (int q = 0; q < 6; ++q) {
+#pragma unroll
+    for (int h = 0; h < CPL; ++h) cf[q][h] = (TI)0;
+  }
+  int cur = -1;
+
+  for (int s0 = 0; s0 < nnei; s0 += kSeg) {
+    const int n = compact<TI, TA>(g, ai, nli, emi, s0, min(nnei, s0 + kSeg), rec, dRi, lane);
+    wave_sync();
+    for (int e0 = 0; e0 < n; e0 += kBatch) {
+      const int nb = min(kBatch, n - e0);
+      for (int b = 0; b < nb; ++b) {
+        const Rec r = rec[e0 + b];
+        const int off = __builtin_amdgcn_readfirstlane(r.off);
+        const int sf = __builtin_amdgcn_readfirstlane(r.slot);
+        const TI* R = emi + (size_t)(sf & (kClamped - 1)) * 4;
+        const TI r0 = R[0], r1 = R[1], r2 = R[2], r3 = R[3];
+        if (off != cur) {
+          cur = off;
+          load_coef<TI, CPL>(coeff + off, ld, c0, cf);
+        }
+        const TI t = (TI)r.t;
+        TA p0 = 0, p1 = 0, p2 = 0, p3 = 0;
+        const bool clamped = (sf & kClamped) != 0;
+#pragma unroll
+        for (int h = 0; h < CPL; ++h) {
+          // value and derivative of the quintic by a joint Horner scheme
+          TI v = cf[5][h], d = cf[5][h];
+          v = fma(v, t, cf[4][h]);
+          d = fma(d, t, v);
+          v = fma(v, t, cf[3][h]);
+          d = fma(d, t, v);
+          v = fma(v, t, cf[2][h]);
+          d = fma(d, t, v);
+          v = fma(v, t, cf[1][h]);
+          d = fma(d, t, v);
+          v = fma(v, t, cf[0][h]);
+          const TA gv = (TA)v;
+          const TA gd = clamped ? (TA)0 : (TA)d;
+          TA w = dt[h][0] * (TA)r0;
+          w = fma(dt[h][1], (TA)r1, w);
+          w = fma(dt[h][2], (TA)r2, w);
+          w = fma(dt[h][3], (TA)r3, w);
+          p0 = fma(dt[h][0], gv, fma(gd, w, p0));
+          p1 = fma(dt[h][1], gv, p1);
+          p2 = fma(dt[h][2], gv, p2);
+          p3 = fma(dt[h][3], gv, p3);
+        }
+        if (owner) {
+          TA* o = red + ((size_t)b * nl + lane) * 4;
+          o[0] = p0;
+          o[1] = p1;
+          o[2] = p2;
+          o[3] = p3;
+        }
       }
-      if (cl) u0 = u1 = u2 = u3 = 0;
-      o0 = v0 + (u0 * (TA)r0 + u1 * (TA)r1 + u2 * (TA)r2 + u3 * (TA)r3);
-      o1 = v1;
-      o2 = v2;
-      o3 = v3;
-    }
-    if (j < nnei) {
-      TA* out = dRi + (size_t)j * 4;
-      out[0] = o0;
-      out[1] = o1;
-      out[2] = o2;
-      out[3] = o3;
+      wave_sync();
+      reduce_batch<TA>(red, nl, nb, rec + e0, dRi, lane);
+      wave_sync();
     }
   }
 }
+
+bool dtype_ok(int dt) { return dt == DPC_F64 || dt == DPC_F32 || dt == DPC_F32_ACC64; }
 
 thread_local hipError_t g_last_hip = hipSuccess;
 
@@ -293,8 +383,6 @@ int launch_status() {
   g_last_hip = e;
   return DPC_EHIP;
 }
-
-bool dtype_ok(int dt) { return dt == DPC_F64 || dt == DPC_F32 || dt == DPC_F32_ACC64; }
 
 // Host-side validation shared by both passes; fills the kernel geometry.
 int make_geo(int nloc, int ntypes, const int* sel, int m1, int m2, const dpc_range* ranges,
@@ -310,12 +398,13 @@ int make_geo(int nloc, int ntypes, const int* sel, int m1, int m2, const dpc_ran
   }
   if (nnei < 1 || nnei > (1 << 20)) return DPC_EINVAL;
   for (int b = ntypes; b < DPC_MAX_TYPES; ++b) g->blk_end[b] = (int)nnei;
+  const int ld = DPC_TABLE_LD(m1);
   for (int p = 0; p < ntypes * ntypes; ++p) {
     const dpc_range& r = ranges[p];
     if (!(std::isfinite(r.lo) && std::isfinite(r.d1) && std::isfinite(r.d2) && r.d1 > 0 &&
           r.d2 > 0 && r.L1 >= 1 && r.L2 >= 1 && r.offset >= 0))
       return DPC_ERANGE;
-    if (r.offset + (r.L1 + r.L2) * 6 * (int64_t)m1 >= (int64_t(1) << 31)) return DPC_ENOTSUP;
+    if (r.offset + (r.L1 + r.L2) * 6 * (int64_t)ld >= (int64_t(1) << 31)) return DPC_ENOTSUP;
     PairRange& q = g->pr[p];
     q.lo = r.lo;
     q.d1 = r.d1;
@@ -330,25 +419,27 @@ int make_geo(int nloc, int ntypes, const int* sel, int m1, int m2, const dpc_ran
   g->ntypes = ntypes;
   g->m1 = m1;
   g->m2 = m2;
+  g->ld = ld;
   return DPC_OK;
 }
+
+// Channels per lane: 1 (m1 <= 64), 2 (m1 <= 128) or 4 (m1 <= 256).
+int channels_per_lane(int m1) { return m1 <= 64 ? 1 : (m1 <= 128 ? 2 : 4); }
 
 template <typename TI, typename TA>
 int launch_fwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype, const int* nlist,
                const void* em, void* T, void* D) {
   const dim3 grid((g.nloc + kWaves - 1) / kWaves), block(64 * kWaves);
-  const size_t shm = (size_t)kWaves * g.m2 * 4 * sizeof(TA) + kWaves * 64 * (sizeof(TI) + 4);
-  const int cpl = (g.m1 + 63) / 64;
+  const size_t shm = (size_t)kWaves * kSeg * sizeof(Rec) + (size_t)kWaves * g.m2 * 4 * sizeof(TA);
   (void)hipGetLastError();  // report only what this launch raises
-  auto args = [&](auto kern) {
+  auto go = [&](auto kern) {
     hipLaunchKernelGGL(kern, grid, block, shm, s, g, (const TI*)coeff, atype, nlist,
                        (const TI*)em, (TA*)T, (TA*)D);
   };
-  switch (cpl) {
-    case 1: args(se_a_fwd_kernel<TI, TA, 1>); break;
-    case 2: args(se_a_fwd_kernel<TI, TA, 2>); break;
-    case 3: args(se_a_fwd_kernel<TI, TA, 3>); break;
-    default: args(se_a_fwd_kernel<TI, TA, 4>); break;
+  switch (channels_per_lane(g.m1)) {
+    case 1: go(se_a_fwd_kernel<TI, TA, 1>); break;
+    case 2: go(se_a_fwd_kernel<TI, TA, 2>); break;
+    default: go(se_a_fwd_kernel<TI, TA, 4>); break;
   }
   return launch_status();
 }
@@ -357,9 +448,20 @@ template <typename TI, typename TA>
 int launch_bwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype, const int* nlist,
                const void* em, const void* dT, void* dR) {
   const dim3 grid((g.nloc + kWaves - 1) / kWaves), block(64 * kWaves);
+  const int cpl = channels_per_lane(g.m1);
+  const int nl = (g.m1 + cpl - 1) / cpl;
+  const size_t shm =
+      (size_t)kWaves * kSeg * sizeof(Rec) + (size_t)kWaves * kBatch * nl * 4 * sizeof(TA);
   (void)hipGetLastError();  // report only what this launch raises
-  hipLaunchKernelGGL((se_a_bwd_kernel<TI, TA>), grid, block, 0, s, g, (const TI*)coeff, atype,
-                     nlist, (const TI*)em, (const TI*)dT, (TA*)dR);
+  auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, grid, block, shm, s, g, (const TI*)coeff, atype, nlist,
+                       (const TI*)em, (const TI*)dT, (TA*)dR);
+  };
+  switch (cpl) {
+    case 1: go(se_a_bwd_kernel<TI, TA, 1>); break;
+    case 2: go(se_a_bwd_kernel<TI, TA, 2>); break;
+    default: go(se_a_bwd_kernel<TI, TA, 4>); break;
+  }
   return launch_status();
 }
 

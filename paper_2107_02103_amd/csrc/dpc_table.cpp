@@ -98,7 +98,7 @@ struct NetEval {
 
 template <typename T>
 void fit_segment(const double* y0, const double* y0p, const double* y0pp, const double* y1,
-                 const double* y1p, const double* y1pp, double dt, int m1, T* out) {
+                 const double* y1p, const double* y1pp, double dt, int m1, int ld, T* out) {
   const double dt2 = dt * dt, dt3 = dt2 * dt, dt4 = dt3 * dt, dt5 = dt4 * dt;
   for (int m = 0; m < m1; ++m) {
     const double A = y1[m] - y0[m] - y0p[m] * dt - 0.5 * y0pp[m] * dt2;
@@ -108,18 +108,21 @@ void fit_segment(const double* y0, const double* y0p, const double* y0pp, const 
     const double b = (-15.0 * A + 7.0 * B * dt - C * dt2) / dt4;
     const double c = (10.0 * A - 4.0 * B * dt + 0.5 * C * dt2) / dt3;
     // row q holds the coefficient of t^q for all channels
-    out[0 * m1 + m] = (T)y0[m];
-    out[1 * m1 + m] = (T)y0p[m];
-    out[2 * m1 + m] = (T)(0.5 * y0pp[m]);
-    out[3 * m1 + m] = (T)c;
-    out[4 * m1 + m] = (T)b;
-    out[5 * m1 + m] = (T)a;
+    out[0 * ld + m] = (T)y0[m];
+    out[1 * ld + m] = (T)y0p[m];
+    out[2 * ld + m] = (T)(0.5 * y0pp[m]);
+    out[3 * ld + m] = (T)c;
+    out[4 * ld + m] = (T)b;
+    out[5 * ld + m] = (T)a;
   }
+  for (int q = 0; q < 6; ++q)
+    for (int m = m1; m < ld; ++m) out[q * ld + m] = (T)0;
 }
 
 template <typename T>
 void build(const dpc_net& net, const dpc_range& r, T* out) {
   const int m1 = net.widths[net.n_layers];
+  const int ld = DPC_TABLE_LD(m1);
   NetEval ev(net);
   std::vector<double> py, pdy, pd2y;
   const double x_up = r.lo + (double)r.L1 * r.d1;
@@ -135,7 +138,7 @@ void build(const dpc_net& net, const dpc_range& r, T* out) {
     for (int64_t q = 1; q <= n; ++q, ++l) {
       ev.run(x0 + (double)q * dt);
       fit_segment<T>(py.data(), pdy.data(), pd2y.data(), ev.y.data(), ev.dy.data(),
-                     ev.d2y.data(), dt, m1, out + (size_t)l * 6 * m1);
+                     ev.d2y.data(), dt, m1, ld, out + (size_t)l * 6 * ld);
       py.swap(ev.y);
       pdy.swap(ev.dy);
       pd2y.swap(ev.d2y);
@@ -154,7 +157,7 @@ extern "C" int dpc_table_layout(int npair, int m1, dpc_range* ranges, dpc_dtype 
     if (!range_ok(ranges[p])) return DPC_ERANGE;
   for (int p = 0; p < npair; ++p) {
     ranges[p].offset = off;
-    off += (ranges[p].L1 + ranges[p].L2) * 6 * (int64_t)m1;
+    off += (ranges[p].L1 + ranges[p].L2) * 6 * (int64_t)DPC_TABLE_LD(m1);
   }
   if (off >= (int64_t(1) << 31)) return DPC_ENOTSUP;  // kernels index with 32-bit offsets
   *total_bytes = (size_t)off * dtype_bytes(dtype);

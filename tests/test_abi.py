@@ -41,8 +41,8 @@ def test_strerror_and_version():
 def test_table_layout_offsets():
     r = P.make_ranges([0.0, -1.0], [0.01, 0.02], [10, 20], [0.1, 0.1], [2, 3], )
     nbytes = P.dpc_table_layout(r, 7, P.DPC_F64)
-    assert r[0].offset == 0 and r[1].offset == 12 * 6 * 7
-    assert nbytes == (12 + 23) * 6 * 7 * 8
+    assert r[0].offset == 0 and r[1].offset == 12 * 6 * 8        # rows padded to 8 channels
+    assert nbytes == (12 + 23) * 6 * 8 * 8
     assert P.dpc_table_layout(r, 7, P.DPC_F32) == nbytes // 2
 
 
@@ -69,7 +69,9 @@ def test_table_layout_rejects_bad_sizes():
 def _eval_lib(buf, rng, m1, x):
     """Value/slope/curvature of the library's table at x (test-side Horner)."""
     L1, L2 = rng.L1, rng.L2
-    c = buf[rng.offset:rng.offset + (L1 + L2) * 6 * m1].reshape(L1 + L2, 6, m1).astype(np.float64)
+    ld = B.table_ld(m1)
+    c = buf[rng.offset:rng.offset + (L1 + L2) * 6 * ld].reshape(L1 + L2, 6, ld)[:, :, :m1]
+    c = c.astype(np.float64)
     x_up = rng.lo + L1 * rng.d1
     l = np.where(x < x_up, np.clip(np.floor((x - rng.lo) / rng.d1), 0, L1 - 1),
                  L1 + np.clip(np.floor((x - x_up) / rng.d2), 0, L2 - 1)).astype(int)
@@ -95,6 +97,13 @@ def test_build_table_matches_oracle_by_evaluation(seed, widths):
     assert np.max(np.abs(g - o)) <= 1e-13 * s
     assert np.max(np.abs(g1 - o1)) <= 1e-9 * np.max(np.abs(o1))
     assert np.max(np.abs(g2 - o2)) <= 1e-5 * np.max(np.abs(o2))
+
+
+def test_table_padding_is_zero():
+    net = random_net(np.random.default_rng(4), (1, 3, 6, 6))    # m1 = 6 -> rows of 8
+    r = P.make_ranges([-0.5], [0.01], [20], [0.1], [2])
+    buf = P.build_tables([net], r, P.DPC_F64).reshape(22, 6, 8)
+    assert np.all(buf[:, :, 6:] == 0) and np.any(buf[:, :, :6] != 0)
 
 
 def test_build_table_f32_is_rounded_f64():
