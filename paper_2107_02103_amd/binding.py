@@ -11,7 +11,8 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "_lib", "libdpc.so")
+# DPC_LIBRARY may name another build of the same library (e.g. a tuning variant).
+LIB_PATH = os.environ.get("DPC_LIBRARY") or os.path.join(_HERE, "_lib", "libdpc.so")
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(
