@@ -8,22 +8,33 @@
 // Mapping (both kernels): lanes = channels.  Lane l owns the CPL consecutive
 // channels CPL*l .. CPL*l + CPL - 1, so one 16-byte buffer load brings the
 // coefficient of t^q for all of them (table rows are padded to a multiple of
-// 4 channels).  A wavefront processes NB atoms together.  Each atom's
-// neighbour list is compacted, 64 slots at a time, into LDS records
-// {t, interval offset, slot}; the wave then merges the NB record streams by
-// interval (largest offset first) with the record, the R~ row (scalar loads)
-// and the interval uniform across the wave.  The coefficients of the current
-// interval stay in registers until the interval changes, so every record of
-// any of the NB atoms that falls into the same interval reuses them:
-// neighbours are distance sorted, and atoms of the same kind see the same
-// distances, so the load traffic per neighbour falls with NB.
+// 4 channels).  A coefficient load costs the vector memory path the same time
+// however many lanes use it, so a wavefront serves NB atoms at once and lets
+// all their neighbours that fall into one interval share the load.
+//
+// Chunk sets: the neighbour lists of the NB atoms are walked in lockstep,
+// 64 / NB slots per atom at a time, so that one pass of 64 lanes covers a
+// chunk set.  Valid slots become records {R~ row, t} plus a key that orders
+// intervals by (neighbour block, decreasing coefficient offset); lists sorted
+// by distance are sorted by key.  The NB sorted lists are merged into one LDS
+// array (rank = own position + binary-search counts in the other lists), in
+// which equal keys form runs and, inside a run, records are grouped by atom;
+// lists that are not sorted are concatenated instead, which is correct but
+// shares less.  Each lane r holds the key, start and per-atom split points of
+// run r; the wave fetches them with v_readlane.
+//
+// The wave walks the runs.  At the start of a run it issues the loads of the
+// next run's coefficients into the second register set (always, so that the
+// wait for the current set is a fixed count), then runs one loop per atom
+// over that atom's records of the run, so accumulators and dE/dT are indexed
+// statically.  Records are read from LDS two at a time.
 //
 // Forward: acc[a][k] += g_m(t) * R~[k] per channel, then T and D = T (T<)^T.
 // Backward: for every record each lane forms its share of
 //   dE/dR~[k] = sum_m dT[m][k] g_m + (k == 0) sum_m g'_m sum_k' dT[m][k'] R~[k']
-// over its channels; the shares of a batch of 8 records are summed across
-// lanes through LDS (each lane adds a strip of the transposed batch, then four
-// strips are combined).
+// over its channels; the shares of a batch of 4 records are summed across
+// lanes through LDS.  Beyond the table g is constant; the record then carries
+// a zero row for the w term, which removes the derivative term.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -41,8 +52,11 @@
 namespace {
 
 constexpr int kWaves = 4;      // wavefronts per workgroup
-constexpr int kChunk = 64;     // neighbour slots compacted at a time (per atom)
-constexpr int kBatch = 8;      // records per cross-lane reduction in the backward pass
+constexpr int kLanes = 64;
+constexpr int kBatch = 4;      // records per cross-lane reduction in the backward pass
+constexpr int kOffBits = 28;   // keys: (block << 28) | (2^28 - 1 - coefficient offset)
+constexpr int kOffMask = (1 << kOffBits) - 1;
+constexpr size_t kMaxLds = 65536;    // LDS a workgroup may take without opting in
 
 struct PairRange {             // one ordered type pair's table, as the kernels see it
   double lo, d1, d2;
@@ -58,13 +72,24 @@ struct Geo {
   PairRange pr[DPC_MAX_TYPES * DPC_MAX_TYPES];
 };
 
+template <typename TI>
 struct Rec {                   // one valid neighbour, as staged in LDS
+  TI r[4];                     // its row of R~ (zero in the backward pass when clamped)
   double t;                    // offset from the left node of its interval
-  int off;                     // element offset of the interval's coefficient rows
-  int slot;                    // neighbour slot; bit 30 set = beyond the table (clamped)
+  double pad;
 };
-constexpr int kClamped = 1 << 30;
-constexpr int kSlotMask = kClamped - 1;
+
+// LDS of one wavefront for one chunk set.
+template <typename TI>
+struct WaveLds {
+  Rec<TI> z[kLanes];           // merged records
+  int mk[kLanes];              // keys in merged order
+  int mi[kLanes];              // slot | atom << 20 in merged order
+  int rk[kLanes + 2];          // run keys (before that: keys of the compacted per-atom lists)
+  int rs[kLanes + 2];          // run starts, then the record count
+};
+
+__host__ __device__ constexpr size_t align16(size_t x) { return (x + 15) & ~size_t(15); }
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v2i __attribute__((ext_vector_type(2)));
@@ -75,6 +100,8 @@ __device__ __forceinline__ int block_of(const Geo& g, int j) {
   for (int k = 0; k < DPC_MAX_TYPES - 1; ++k) b += (k < g.ntypes - 1 && j >= g.blk_end[k]) ? 1 : 0;
   return b;
 }
+
+__device__ __forceinline__ int key_offset(int key) { return kOffMask - (key & kOffMask); }
 
 // Interval of x in one pair's table (see dpc_range in dpc.h).  Always float64.
 __device__ __forceinline__ void locate(const PairRange& P, double x, int& l, double& t,
@@ -110,85 +137,19 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
                                    __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
 }
 
-// Compact the valid slots [s0, s1) (at most 64) of one atom into records;
-// returns their count.  Invalid slots get a zero row in `zero_out` if given.
-template <typename TI, typename TA>
-__device__ __forceinline__ int compact(const Geo& g, int ai, const int* nli, const TI* emi,
-                                       int s0, int s1, Rec* rec, TA* zero_out, int lane) {
-  const int j = s0 + lane;
-  bool valid = false;
-  Rec r;
-  if (j < s1) {
-    valid = nli[j] >= 0;
-    if (valid) {
-      const PairRange& P = g.pr[ai * g.ntypes + block_of(g, j)];
-      int l;
-      bool cl;
-      locate(P, (double)emi[(size_t)j * 4], l, r.t, cl);
-      r.off = P.offset + l * 6 * g.ld;
-      r.slot = j | (cl ? kClamped : 0);
-    } else if (zero_out) {
-      TA* o = zero_out + (size_t)j * 4;
-      o[0] = o[1] = o[2] = o[3] = (TA)0;
-    }
-  }
-  const uint64_t mask = __ballot(valid);
-  if (valid) rec[lanes_below(mask)] = r;
-  return __popcll(mask);
-}
-
-// Record stream of one atom: its current chunk of records in LDS and the
-// head record (uniform values).
-template <typename TI>
-struct Stream {
-  int ai;      // atom type, or -1 when the atom is absent or finished
-  int next;    // first slot not compacted yet
-  int n, c;    // records in the chunk, cursor
-  int head;    // coefficient offset of the head record, -1 when exhausted
-  int slot;    // slot (and clamp bit) of the head record
-  TI t;        // offset of the head record
-};
-
-template <typename TI>
-__device__ __forceinline__ void read_head(Stream<TI>& s, const Rec* rec) {
-  const Rec r = rec[s.c];
-  s.head = __builtin_amdgcn_readfirstlane(r.off);
-  s.slot = __builtin_amdgcn_readfirstlane(r.slot);
-  s.t = (TI)r.t;
-}
-
-// Move to the next record, compacting further chunks as needed.
-template <typename TI, typename TA>
-__device__ __forceinline__ void advance(Stream<TI>& s, const Geo& g, const int* nli,
-                                        const TI* emi, Rec* rec, TA* zero_out, int lane) {
-  if (++s.c < s.n) {
-    read_head(s, rec);
-    return;
-  }
-  while (s.next < g.nnei) {
-    wave_sync();
-    const int n = compact<TI, TA>(g, s.ai, nli, emi, s.next, min(g.nnei, s.next + kChunk), rec,
-                                  zero_out, lane);
-    s.next += kChunk;
-    if (n > 0) {
-      wave_sync();
-      s.n = n;
-      s.c = 0;
-      read_head(s, rec);
-      return;
-    }
-  }
-  s.head = -1;
+__device__ __forceinline__ int readlane(int v, int lane) {
+  return __builtin_amdgcn_readlane(v, lane);
 }
 
 template <typename TI>
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t coeff_rsrc(const TI* coeff, int bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc((void*)coeff, (short)0, bytes, 0x00020000);
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const TI* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)p, (short)0, bytes, 0x00020000);
 }
 
-// Coefficients of t^q (q = 0..5) of the lane's CPL channels in the interval
-// whose rows start at element `off`.  voff = byte offset of the lane's first
-// channel inside a row.
+// Coefficients of t^q (q = 0..5) of the lane's CPL channels of the interval
+// whose rows start at element `off`; voff = byte offset of the lane's first
+// channel inside a row.  Every lane loads (lanes without channels read the
+// last row entries again), so the number of loads in flight is fixed.
 template <typename TI, int CPL>
 __device__ __forceinline__ void load_coef(__amdgpu_buffer_rsrc_t rs, int off, int ld, int voff,
                                           TI (&cf)[6][CPL]) {
@@ -228,28 +189,177 @@ __device__ __forceinline__ void load_coef(__amdgpu_buffer_rsrc_t rs, int off, in
 }
 
 // ---------------------------------------------------------------------------
+// Chunk sets (shared by both passes)
+// ---------------------------------------------------------------------------
+struct Tables {
+  int n, nruns;                // records and runs of the chunk set
+  int vs;                      // lane r: start of run r (n for r >= nruns)
+  int vk;                      // lane r: key of run min(r, nruns - 1)
+  int vp[2];                   // lane r: first record of atoms 1..NB-1 in run r, 8 bits each
+};
+
+// First record of atom b (0 < b < NB) in a run, from its packed split points.
+template <int NB>
+__device__ __forceinline__ int split_at(const int (&p)[2], int b) {
+  return (p[(b - 1) >> 2] >> (8 * ((b - 1) & 3))) & 255;
+}
+
+// Merge slots [s0, s0 + 64/NB) of the wave's NB atoms into W and build the
+// run tables.  In the backward pass (kBwd) padded slots get a zero output row
+// and clamped records a zero R~ row.
+template <typename TI, typename TA, int NB, bool kBwd>
+__device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[NB], int i0,
+                                                  int s0, const int* __restrict__ nlist,
+                                                  const TI* __restrict__ em, WaveLds<TI>& W,
+                                                  TA* __restrict__ dR, int lane) {
+  constexpr int kC = kLanes / NB;
+  const int a = lane / kC, sl = lane % kC, j = s0 + sl;
+  int at = -1;
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+    if (b == a) at = ai[b];
+  bool valid = false;
+  Rec<TI> rec;
+  int key = 0;
+  if (at >= 0 && j < g.nnei) {
+    const size_t row = (size_t)(i0 + a) * g.nnei + j;
+    valid = nlist[row] >= 0;
+    if (valid) {
+      const TI* e = em + row * 4;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) rec.r[k] = e[k];
+      const int blk = block_of(g, j);
+      const PairRange& P = g.pr[at * g.ntypes + blk];
+      int l;
+      bool cl;
+      locate(P, (double)rec.r[0], l, rec.t, cl);
+      rec.pad = 0.0;
+      key = (blk << kOffBits) | (kOffMask - (P.offset + l * 6 * g.ld));
+      if (kBwd && cl) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) rec.r[k] = (TI)0;
+      }
+    } else if constexpr (kBwd) {
+      TA* o = dR + row * 4;
+      o[0] = o[1] = o[2] = o[3] = (TA)0;
+    }
+  }
+  const uint64_t m = __ballot(valid);
+  if (m == 0) return Tables{0, 0, 0, 0, {0, 0}};
+  const uint64_t seg = kC == 64 ? ~0ull : ((1ull << kC) - 1);
+  const uint64_t before_seg = a == 0 ? 0ull : ((1ull << (a * kC)) - 1);
+  const int pos = lanes_below(m) - __popcll(m & before_seg);
+  int r = pos;
+  if constexpr (NB > 1) {
+    int* lk = W.rk;            // free until the run tables are written
+    if (valid) lk[a * kC + pos] = key;
+    wave_sync();
+    const int cnt_a = __popcll((m >> (a * kC)) & seg);
+    bool bad = false;
+    if (sl + 1 < cnt_a) bad = lk[lane] > lk[lane + 1];
+    const bool sorted = __ballot(bad) == 0;
+    if (valid) {
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const int cnt_b = __popcll((m >> (b * kC)) & seg);
+        if (sorted) {
+          // records of list b that come first: smaller key, or equal key of a lower atom
+          const int* kb = lk + b * kC;
+          int c = 0;
+#pragma unroll
+          for (int step = kC; step > 0; step >>= 1) {
+            if (c + step <= cnt_b) {
+              const int kk = kb[c + step - 1];
+              if (b < a ? kk <= key : kk < key) c += step;
+            }
+          }
+          r += b == a ? 0 : c;
+        } else {
+          r += b < a ? cnt_b : 0;
+        }
+      }
+    }
+  }
+  if (valid) {
+    W.z[r] = rec;
+    W.mk[r] = key;
+    W.mi[r] = j | (a << 20);
+  }
+  wave_sync();
+
+  Tables T;
+  T.n = __popcll(m);
+  const bool in = lane < T.n;
+  const int ke = W.mk[lane], ae = (W.mi[lane] >> 20) & 7;
+  const int kp = W.mk[lane > 0 ? lane - 1 : 0];
+  const bool f = in && (lane == 0 || ke != kp);
+  const uint64_t F = __ballot(f);
+  T.nruns = __popcll(F);
+  if (f) {
+    const int rr = lanes_below(F);
+    W.rk[rr] = ke;
+    W.rs[rr] = lane;
+  }
+  if (lane == 0) W.rs[T.nruns] = T.n;
+  wave_sync();
+  const int S = W.rs[min(lane, T.nruns)], E = W.rs[min(lane + 1, T.nruns)];
+  T.vs = S;
+  T.vk = W.rk[min(lane, max(T.nruns - 1, 0))];
+  // records of run r are [S, E); inside it atoms come in increasing order
+  const uint64_t run_mask = (E >= 64 ? ~0ull : ((1ull << E) - 1)) & ~(S >= 64 ? ~0ull : ((1ull << S) - 1));
+  T.vp[0] = T.vp[1] = 0;
+#pragma unroll
+  for (int b = 1; b < NB; ++b) {
+    const uint64_t below = __ballot(in && ae < b);
+    const int p = S + __popcll(below & run_mask);
+    T.vp[(b - 1) >> 2] |= p << (8 * ((b - 1) & 3));
+  }
+  wave_sync();
+  return T;
+}
+
+// ---------------------------------------------------------------------------
 // forward: T and D
 // ---------------------------------------------------------------------------
+template <typename TI, typename TA>
+__host__ __device__ constexpr size_t fwd_wave_bytes(int m2) {
+  return align16(sizeof(WaveLds<TI>)) + align16((size_t)m2 * 4 * sizeof(TA));
+}
+
 template <typename TI, typename TA, int CPL, int NB>
 __global__ __launch_bounds__(64 * kWaves) void se_a_fwd_kernel(
     const Geo g, const TI* __restrict__ coeff, const int* __restrict__ atype,
     const int* __restrict__ nlist, const TI* __restrict__ em, TA* __restrict__ T,
     TA* __restrict__ D) {
   extern __shared__ __align__(16) unsigned char smem[];
+  constexpr int kC = kLanes / NB;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int i0 = __builtin_amdgcn_readfirstlane((blockIdx.x * kWaves + wave) * NB);
   if (i0 >= g.nloc) return;
   const int nnei = g.nnei, m1 = g.m1, m2 = g.m2, ld = g.ld;
-  Rec* rec0 = reinterpret_cast<Rec*>(smem) + (size_t)wave * NB * kChunk;
-  TA* sT = reinterpret_cast<TA*>(reinterpret_cast<Rec*>(smem) + kWaves * NB * kChunk) +
-           (size_t)wave * m2 * 4;
-  const __amdgpu_buffer_rsrc_t rs = coeff_rsrc(coeff, g.coeff_bytes);
-  const int c0 = min(lane * CPL, ld - CPL);
-  const int voff = c0 * (int)sizeof(TI);
-  const bool owner = lane * CPL < m1;
+  unsigned char* wb = smem + wave * fwd_wave_bytes<TI, TA>(m2);
+  WaveLds<TI>& W = *reinterpret_cast<WaveLds<TI>*>(wb);
+  TA* sT = reinterpret_cast<TA*>(wb + align16(sizeof(WaveLds<TI>)));
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(coeff, g.coeff_bytes);
+  const int voff = min(lane * CPL, ld - CPL) * (int)sizeof(TI);
 
-  Stream<TI> st[NB];
+  int ai[NB];
+#pragma unroll
+  for (int a = 0; a < NB; ++a) {
+    const int i = i0 + a;
+    ai[a] = -1;
+    if (i < g.nloc) {
+      const int t = __builtin_amdgcn_readfirstlane(atype[i]);
+      if (t < 0 || t >= g.ntypes) {  // invalid type: the atom's outputs become NaN
+        const TA nan = (TA)NAN;
+        for (int e = lane; e < m1 * 4; e += 64) T[(size_t)i * m1 * 4 + e] = nan;
+        for (int e = lane; e < m1 * m2; e += 64) D[(size_t)i * m1 * m2 + e] = nan;
+      } else {
+        ai[a] = t;
+      }
+    }
+  }
   TA acc[NB][CPL][4];
 #pragma unroll
   for (int a = 0; a < NB; ++a) {
@@ -258,77 +368,68 @@ __global__ __launch_bounds__(64 * kWaves) void se_a_fwd_kernel(
 #pragma unroll
       for (int k = 0; k < 4; ++k) acc[a][h][k] = (TA)0;
     }
-    const int i = i0 + a;
-    st[a].ai = -1;
-    st[a].head = -1;
-    st[a].next = 0;
-    st[a].n = st[a].c = 0;
-    st[a].slot = 0;
-    st[a].t = (TI)0;
-    if (i < g.nloc) {
-      const int ai = __builtin_amdgcn_readfirstlane(atype[i]);
-      if (ai < 0 || ai >= g.ntypes) {  // invalid type: the atom's outputs become NaN
-        const TA nan = (TA)NAN;
-        for (int e = lane; e < m1 * 4; e += 64) T[(size_t)i * m1 * 4 + e] = nan;
-        for (int e = lane; e < m1 * m2; e += 64) D[(size_t)i * m1 * m2 + e] = nan;
-      } else {
-        st[a].ai = ai;
-        st[a].c = -1;
-        advance<TI, TA>(st[a], g, nlist + (size_t)i * nnei, em + (size_t)i * nnei * 4,
-                        rec0 + a * kChunk, nullptr, lane);
-      }
-    }
   }
+  TI cfA[6][CPL], cfB[6][CPL];
 
-  TI cf[6][CPL];
-#pragma unroll
-  for (int q = 0; q < 6; ++q) {
-#pragma unroll
-    for (int h = 0; h < CPL; ++h) cf[q][h] = (TI)0;
-  }
-  int cur = -1;
-  for (;;) {
-    int key = st[0].head;
-#pragma unroll
-    for (int a = 1; a < NB; ++a) key = max(key, st[a].head);
-    if (key < 0) break;
-    if (key != cur) {
-      cur = key;
-      if (owner) load_coef<TI, CPL>(rs, key, ld, voff, cf);
-    }
-#pragma unroll
-    for (int a = 0; a < NB; ++a) {
-      const TI* emi = em + (size_t)(i0 + a) * nnei * 4;
-      while (st[a].head == key) {
-        const TI* R = emi + (size_t)(st[a].slot & kSlotMask) * 4;
-        const TI r0 = R[0], r1 = R[1], r2 = R[2], r3 = R[3];
-        const TI t = st[a].t;
+  for (int s0 = 0; s0 < nnei; s0 += kC) {
+    const Tables tb = build_chunk_set<TI, TA, NB, false>(g, ai, i0, s0, nlist, em, W,
+                                                         (TA*)nullptr, lane);
+    if (tb.n == 0) continue;
+    load_coef<TI, CPL>(rs, key_offset(readlane(tb.vk, 0)), ld, voff, cfA);
+    int r = 0;
+    // run r with `cur` loaded; the next run's coefficients go to `nxt`
+    auto run = [&](TI (&cur)[6][CPL], TI (&nxt)[6][CPL]) __attribute__((always_inline)) {
+      load_coef<TI, CPL>(rs, key_offset(readlane(tb.vk, min(r + 1, kLanes - 1))), ld, voff,
+                         nxt);
+      const int S = readlane(tb.vs, r);
+      const int E = r + 1 < kLanes ? readlane(tb.vs, r + 1) : tb.n;
+      int p[2] = {0, 0};
+      if constexpr (NB > 1) p[0] = readlane(tb.vp[0], r);
+      if constexpr (NB > 5) p[1] = readlane(tb.vp[1], r);
+      auto one = [&](const Rec<TI>& c, auto& ac) __attribute__((always_inline)) {
+        const TI t = (TI)c.t;
 #pragma unroll
         for (int h = 0; h < CPL; ++h) {
-          TI gv = cf[5][h];
-          gv = fma(gv, t, cf[4][h]);
-          gv = fma(gv, t, cf[3][h]);
-          gv = fma(gv, t, cf[2][h]);
-          gv = fma(gv, t, cf[1][h]);
-          gv = fma(gv, t, cf[0][h]);
-          const TA ga = (TA)gv;
-          acc[a][h][0] = fma(ga, (TA)r0, acc[a][h][0]);
-          acc[a][h][1] = fma(ga, (TA)r1, acc[a][h][1]);
-          acc[a][h][2] = fma(ga, (TA)r2, acc[a][h][2]);
-          acc[a][h][3] = fma(ga, (TA)r3, acc[a][h][3]);
+          TI v = cur[5][h];
+          v = fma(v, t, cur[4][h]);
+          v = fma(v, t, cur[3][h]);
+          v = fma(v, t, cur[2][h]);
+          v = fma(v, t, cur[1][h]);
+          v = fma(v, t, cur[0][h]);
+#pragma unroll
+          for (int k = 0; k < 4; ++k) ac[h][k] = fma((TA)v, (TA)c.r[k], ac[h][k]);
         }
-        advance<TI, TA>(st[a], g, nlist + (size_t)(i0 + a) * nnei, emi, rec0 + a * kChunk,
-                        nullptr, lane);
+      };
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const int lo = b == 0 ? S : split_at<NB>(p, b);
+        const int hi = b == NB - 1 ? E : split_at<NB>(p, b + 1);
+        int e = lo;
+        for (; e + 1 < hi; e += 2) {
+          const Rec<TI> c0 = W.z[e], c1 = W.z[e + 1];
+          one(c0, acc[b]);
+          one(c1, acc[b]);
+        }
+        if (e < hi) {
+          const Rec<TI> c0 = W.z[e];
+          one(c0, acc[b]);
+        }
       }
+    };
+    for (;;) {
+      run(cfA, cfB);
+      if (++r == tb.nruns) break;
+      run(cfB, cfA);
+      if (++r == tb.nruns) break;
     }
+    wave_sync();
   }
 
   // T rows and D = T (T<)^T of each atom
 #pragma unroll
   for (int a = 0; a < NB; ++a) {
     const int i = i0 + a;
-    if (i >= g.nloc || st[a].ai < 0) continue;
-    wave_sync();
+    if (ai[a] < 0) continue;
 #pragma unroll
     for (int h = 0; h < CPL; ++h) {
       const int m = lane * CPL + h;
@@ -349,70 +450,43 @@ __global__ __launch_bounds__(64 * kWaves) void se_a_fwd_kernel(
       if (m < m1) {
         TA* Dm = D + ((size_t)i * m1 + m) * m2;
         for (int n = 0; n < m2; ++n) {
-          TA s = acc[a][h][0] * sT[n * 4 + 0];
-          s = fma(acc[a][h][1], sT[n * 4 + 1], s);
-          s = fma(acc[a][h][2], sT[n * 4 + 2], s);
-          s = fma(acc[a][h][3], sT[n * 4 + 3], s);
-          Dm[n] = s;
+          TA v = acc[a][h][0] * sT[n * 4 + 0];
+          v = fma(acc[a][h][1], sT[n * 4 + 1], v);
+          v = fma(acc[a][h][2], sT[n * 4 + 2], v);
+          v = fma(acc[a][h][3], sT[n * 4 + 3], v);
+          Dm[n] = v;
         }
       }
     }
+    wave_sync();
   }
 }
 
 // ---------------------------------------------------------------------------
 // backward: dE/dR~
 // ---------------------------------------------------------------------------
-// LDS of one wave for the cross-lane sums: for each of the kBatch buffered
-// records b and component pair kk, a block of nlq*4 lanes x 16 bytes holding
-// (share[2kk], share[2kk+1]) of every lane (zero for lanes without channels);
-// blocks are 64 bytes past a multiple of 256 apart so that 16 lanes reading
-// 16 bytes each touch every bank once.
-__host__ __device__ constexpr int red_block_bytes(int nlq) {
-  return 64 * nlq + ((64 - (64 * nlq) % 256) % 256 + 256) % 256;
+// Cross-lane sums.  Record b of a batch writes (share[0], share[1]) of every
+// lane to block 2b and (share[2], share[3]) to block 2b + 1, 16 bytes per
+// lane, 64 lanes per block.  Blocks are kRedBlock = 1152 bytes apart (128 past
+// a multiple of 256), so that the 16 lanes of two neighbouring blocks reading
+// 16 bytes each touch every bank once.  Lanes without channels hold zeros
+// (their dE/dT is zero), or NaN when the record is NaN, which then is NaN
+// anyway.  Step 1: lane (G, x) = (lane / 8, lane % 8) adds strip x (lanes x,
+// x + 8, ...) of block G; step 2: the 8 strips of each of the 16 sums are
+// added by lane s = 4b + k, reading a row padded to 16 bytes past a multiple
+// of 64 (no bank repeats).  The step 2 rows reuse the start of the blocks.
+constexpr int kRedBlock = 1152;
+template <typename TA>
+__host__ __device__ constexpr int part_stride() {  // row of step 2, in TA units
+  return 8 + 16 / (int)sizeof(TA);
+}
+template <typename TI>
+__host__ __device__ constexpr size_t bwd_wave_bytes() {
+  return align16(sizeof(WaveLds<TI>)) + (size_t)2 * kBatch * kRedBlock;
 }
 
 template <typename TA>
-struct RedLds {
-  unsigned char* red;   // 2 * kBatch blocks
-  TA* part;             // [16 groups][4 lanes][2] partial sums
-  int* row;             // [kBatch] (atom within the wave) << 21 | slot of each buffered record
-};
-
-// Sum the shares of nb buffered records and write dE/dR~ rows.  Lane L adds
-// the strip x = L % 4 (lanes x, x+4, ...) of block (b, kk) = (L / 8, (L / 4) % 2);
-// the four strips of a block are then combined by lane x = 0.
-template <typename TA, int NLQ>
-__device__ __forceinline__ void reduce_batch(const RedLds<TA>& r, int nlq, int blk, int nb,
-                                             TA* dR, int i0, int nnei, int lane) {
-  const int G = lane >> 2, x = lane & 3, b = G >> 1, kk = G & 1;
-  wave_sync();
-  const unsigned char* base = r.red + (size_t)(b * 2 + kk) * blk + x * 16;
-  TA s0 = 0, s1 = 0;
-#pragma unroll
-  for (int q = 0; q < NLQ; ++q) {
-    if (q < nlq) {
-      const TA* v = reinterpret_cast<const TA*>(base + q * 64);
-      s0 += v[0];
-      s1 += v[1];
-    }
-  }
-  r.part[(G * 4 + x) * 2 + 0] = s0;
-  r.part[(G * 4 + x) * 2 + 1] = s1;
-  wave_sync();
-  if (x == 0 && b < nb) {
-#pragma unroll
-    for (int y = 1; y < 4; ++y) {
-      s0 += r.part[(G * 4 + y) * 2 + 0];
-      s1 += r.part[(G * 4 + y) * 2 + 1];
-    }
-    const int packed = r.row[b];
-    TA* o = dR + ((size_t)(i0 + (packed >> 21)) * nnei + (packed & ((1 << 21) - 1))) * 4 + 2 * kk;
-    o[0] = s0;
-    o[1] = s1;
-  }
-  wave_sync();
-}
+using Pair = TA __attribute__((ext_vector_type(2)));
 
 template <typename TI, typename TA, int CPL, int NB>
 __global__ __launch_bounds__(64 * kWaves) void se_a_bwd_kernel(
@@ -420,37 +494,30 @@ __global__ __launch_bounds__(64 * kWaves) void se_a_bwd_kernel(
     const int* __restrict__ nlist, const TI* __restrict__ em, const TI* __restrict__ dT,
     TA* __restrict__ dR) {
   extern __shared__ __align__(16) unsigned char smem[];
-  constexpr int NLQ = (64 + 3) / 4;            // strips of at most 64 lanes
+  constexpr int kC = kLanes / NB;
+  constexpr int PS = part_stride<TA>();
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int i0 = __builtin_amdgcn_readfirstlane((blockIdx.x * kWaves + wave) * NB);
   if (i0 >= g.nloc) return;
   const int nnei = g.nnei, m1 = g.m1, ld = g.ld;
-  const int nl = (m1 + CPL - 1) / CPL;          // lanes that own channels
-  const int nlq = (nl + 3) / 4;
-  const int blk = red_block_bytes(nlq);
-  const size_t wave_bytes = (size_t)NB * kChunk * sizeof(Rec) + 2 * kBatch * blk +
-                            16 * 4 * 2 * sizeof(TA) + kBatch * sizeof(int);
-  unsigned char* wbase = smem + wave * wave_bytes;
-  Rec* rec0 = reinterpret_cast<Rec*>(wbase);
-  RedLds<TA> rl;
-  rl.red = wbase + (size_t)NB * kChunk * sizeof(Rec);
-  rl.part = reinterpret_cast<TA*>(rl.red + 2 * kBatch * blk);
-  rl.row = reinterpret_cast<int*>(rl.part + 16 * 4 * 2);
-  const __amdgpu_buffer_rsrc_t rs = coeff_rsrc(coeff, g.coeff_bytes);
-  const int c0 = min(lane * CPL, ld - CPL);
-  const int voff = c0 * (int)sizeof(TI);
-  const bool owner = lane < nl;
+  static_assert(16 * part_stride<TA>() * sizeof(TA) <= 2 * kBatch * kRedBlock, "step 2 rows");
+  unsigned char* wb = smem + wave * bwd_wave_bytes<TI>();
+  WaveLds<TI>& W = *reinterpret_cast<WaveLds<TI>*>(wb);
+  unsigned char* red = wb + align16(sizeof(WaveLds<TI>));
+  TA* part = reinterpret_cast<TA*>(red);
+  unsigned char* const wlane = red + lane * 16;                          // record writes
+  const unsigned char* const rlane =
+      red + (lane >> 4) * 2 * kRedBlock + ((lane >> 3) & 1) * kRedBlock + (lane & 7) * 16;
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(coeff, g.coeff_bytes);
+  const int voff = min(lane * CPL, ld - CPL) * (int)sizeof(TI);
 
-  // lanes without channels contribute zeros: clear the whole sum area once
-  for (int e = lane; e < 2 * kBatch * blk / 16; e += 64)
-    reinterpret_cast<v4i*>(rl.red)[e] = (v4i){0, 0, 0, 0};
-
-  Stream<TI> st[NB];
   TA dt[NB][CPL][4];
+  int ai[NB];
 #pragma unroll
   for (int a = 0; a < NB; ++a) {
     const int i = i0 + a;
+    ai[a] = -1;
 #pragma unroll
     for (int h = 0; h < CPL; ++h) {
       const int m = lane * CPL + h;
@@ -458,110 +525,125 @@ __global__ __launch_bounds__(64 * kWaves) void se_a_bwd_kernel(
       for (int k = 0; k < 4; ++k)
         dt[a][h][k] = (i < g.nloc && m < m1) ? (TA)dT[((size_t)i * m1 + m) * 4 + k] : (TA)0;
     }
-    st[a].ai = -1;
-    st[a].head = -1;
-    st[a].next = 0;
-    st[a].n = st[a].c = 0;
-    st[a].slot = 0;
-    st[a].t = (TI)0;
     if (i < g.nloc) {
-      const int ai = __builtin_amdgcn_readfirstlane(atype[i]);
-      if (ai < 0 || ai >= g.ntypes) {  // invalid type: the atom's outputs become NaN
+      const int t = __builtin_amdgcn_readfirstlane(atype[i]);
+      if (t < 0 || t >= g.ntypes) {  // invalid type: the atom's outputs become NaN
         for (int e = lane; e < nnei * 4; e += 64) dR[(size_t)i * nnei * 4 + e] = (TA)NAN;
       } else {
-        st[a].ai = ai;
-        st[a].c = -1;
-        advance<TI, TA>(st[a], g, nlist + (size_t)i * nnei, em + (size_t)i * nnei * 4,
-                        rec0 + a * kChunk, dR + (size_t)i * nnei * 4, lane);
+        ai[a] = t;
       }
     }
   }
-
-  TI cf[6][CPL];
-#pragma unroll
-  for (int q = 0; q < 6; ++q) {
-#pragma unroll
-    for (int h = 0; h < CPL; ++h) cf[q][h] = (TI)0;
-  }
-  int cur = -1;
+  TI cfA[6][CPL], cfB[6][CPL];
   int nb = 0;
-  for (;;) {
-    int key = st[0].head;
+
+  // sum the shares of the nbat records starting at merged position e0
+  auto reduce = [&](int e0, int nbat) __attribute__((always_inline)) {
+    wave_sync();
+    Pair<TA> v[8];
 #pragma unroll
-    for (int a = 1; a < NB; ++a) key = max(key, st[a].head);
-    if (key < 0) break;
-    if (key != cur) {
-      cur = key;
-      if (owner) load_coef<TI, CPL>(rs, key, ld, voff, cf);
+    for (int q = 0; q < 8; ++q) v[q] = *reinterpret_cast<const Pair<TA>*>(rlane + q * 128);
+    Pair<TA> sum = v[0];
+#pragma unroll
+    for (int q = 1; q < 8; ++q) sum += v[q];
+    wave_sync();
+    const int G = lane >> 3, x = lane & 7;
+    part[(2 * G) * PS + x] = sum.x;
+    part[(2 * G + 1) * PS + x] = sum.y;
+    wave_sync();
+    if (lane < 4 * nbat) {
+      // the batch's records have been read: their LDS slots take the results
+      const Pair<TA>* pr = reinterpret_cast<const Pair<TA>*>(part + lane * PS);
+      const Pair<TA> a = pr[0] + pr[1], b = pr[2] + pr[3];
+      reinterpret_cast<TA*>(&W.z[e0 + (lane >> 2)])[lane & 3] = (a.x + a.y) + (b.x + b.y);
     }
-#pragma unroll
-    for (int a = 0; a < NB; ++a) {
-      const TI* emi = em + (size_t)(i0 + a) * nnei * 4;
-      while (st[a].head == key) {
-        const int slot = st[a].slot & kSlotMask;
-        const TI* R = emi + (size_t)slot * 4;
-        const TI r0 = R[0], r1 = R[1], r2 = R[2], r3 = R[3];
-        const TI t = st[a].t;
+    wave_sync();
+  };
+  static_assert(4 * sizeof(TA) <= sizeof(Rec<TI>), "a record slot holds one output row");
+
+  for (int s0 = 0; s0 < nnei; s0 += kC) {
+    const Tables tb = build_chunk_set<TI, TA, NB, true>(g, ai, i0, s0, nlist, em, W, dR, lane);
+    if (tb.n == 0) continue;
+    load_coef<TI, CPL>(rs, key_offset(readlane(tb.vk, 0)), ld, voff, cfA);
+    int r = 0;
+    auto run = [&](TI (&cur)[6][CPL], TI (&nxt)[6][CPL]) __attribute__((always_inline)) {
+      load_coef<TI, CPL>(rs, key_offset(readlane(tb.vk, min(r + 1, kLanes - 1))), ld, voff,
+                         nxt);
+      const int S = readlane(tb.vs, r);
+      const int E = r + 1 < kLanes ? readlane(tb.vs, r + 1) : tb.n;
+      int p[2] = {0, 0};
+      if constexpr (NB > 1) p[0] = readlane(tb.vp[0], r);
+      if constexpr (NB > 5) p[1] = readlane(tb.vp[1], r);
+      auto one = [&](const Rec<TI>& c, const auto& dtb, int e) __attribute__((always_inline)) {
+        const TI t = (TI)c.t;
         TA p0 = 0, p1 = 0, p2 = 0, p3 = 0;
-        if ((st[a].slot & kClamped) == 0) {
 #pragma unroll
-          for (int h = 0; h < CPL; ++h) {
-            // value and derivative of the quintic by a joint Horner scheme
-            TI v = cf[5][h], d = cf[5][h];
-            v = fma(v, t, cf[4][h]);
-            d = fma(d, t, v);
-            v = fma(v, t, cf[3][h]);
-            d = fma(d, t, v);
-            v = fma(v, t, cf[2][h]);
-            d = fma(d, t, v);
-            v = fma(v, t, cf[1][h]);
-            d = fma(d, t, v);
-            v = fma(v, t, cf[0][h]);
-            const TA gv = (TA)v, gd = (TA)d;
-            TA w = dt[a][h][0] * (TA)r0;
-            w = fma(dt[a][h][1], (TA)r1, w);
-            w = fma(dt[a][h][2], (TA)r2, w);
-            w = fma(dt[a][h][3], (TA)r3, w);
-            p0 = fma(dt[a][h][0], gv, fma(gd, w, p0));
-            p1 = fma(dt[a][h][1], gv, p1);
-            p2 = fma(dt[a][h][2], gv, p2);
-            p3 = fma(dt[a][h][3], gv, p3);
-          }
-        } else {  // beyond the table: constant value, zero derivative
-#pragma unroll
-          for (int h = 0; h < CPL; ++h) {
-            TI v = cf[5][h];
-            v = fma(v, t, cf[4][h]);
-            v = fma(v, t, cf[3][h]);
-            v = fma(v, t, cf[2][h]);
-            v = fma(v, t, cf[1][h]);
-            v = fma(v, t, cf[0][h]);
-            const TA gv = (TA)v;
-            p0 = fma(dt[a][h][0], gv, p0);
-            p1 = fma(dt[a][h][1], gv, p1);
-            p2 = fma(dt[a][h][2], gv, p2);
-            p3 = fma(dt[a][h][3], gv, p3);
-          }
+        for (int h = 0; h < CPL; ++h) {
+          // value and derivative of the quintic by a joint Horner scheme
+          TI v = cur[5][h], d = cur[5][h];
+          v = fma(v, t, cur[4][h]);
+          d = fma(d, t, v);
+          v = fma(v, t, cur[3][h]);
+          d = fma(d, t, v);
+          v = fma(v, t, cur[2][h]);
+          d = fma(d, t, v);
+          v = fma(v, t, cur[1][h]);
+          d = fma(d, t, v);
+          v = fma(v, t, cur[0][h]);
+          TA w = dtb[h][0] * (TA)c.r[0];
+          w = fma(dtb[h][1], (TA)c.r[1], w);
+          w = fma(dtb[h][2], (TA)c.r[2], w);
+          w = fma(dtb[h][3], (TA)c.r[3], w);
+          p0 = fma(dtb[h][0], (TA)v, fma((TA)d, w, p0));
+          p1 = fma(dtb[h][1], (TA)v, p1);
+          p2 = fma(dtb[h][2], (TA)v, p2);
+          p3 = fma(dtb[h][3], (TA)v, p3);
         }
-        if (owner) {
-          TA* o0 = reinterpret_cast<TA*>(rl.red + (size_t)(nb * 2 + 0) * blk + lane * 16);
-          TA* o1 = reinterpret_cast<TA*>(rl.red + (size_t)(nb * 2 + 1) * blk + lane * 16);
-          o0[0] = p0;
-          o0[1] = p1;
-          o1[0] = p2;
-          o1[1] = p3;
-        }
-        if (lane == 0) rl.row[nb] = (a << 21) | slot;
+        unsigned char* o = wlane + nb * (2 * kRedBlock);
+        *reinterpret_cast<Pair<TA>*>(o) = Pair<TA>{p0, p1};
+        *reinterpret_cast<Pair<TA>*>(o + kRedBlock) = Pair<TA>{p2, p3};
         if (++nb == kBatch) {
-          reduce_batch<TA, NLQ>(rl, nlq, blk, nb, dR, i0, nnei, lane);
+          reduce(e + 1 - kBatch, kBatch);
           nb = 0;
         }
-        advance<TI, TA>(st[a], g, nlist + (size_t)(i0 + a) * nnei, emi, rec0 + a * kChunk,
-                        dR + (size_t)(i0 + a) * nnei * 4, lane);
+      };
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const int lo = b == 0 ? S : split_at<NB>(p, b);
+        const int hi = b == NB - 1 ? E : split_at<NB>(p, b + 1);
+        int e = lo;
+        for (; e + 1 < hi; e += 2) {
+          const Rec<TI> c0 = W.z[e], c1 = W.z[e + 1];
+          one(c0, dt[b], e);
+          one(c1, dt[b], e + 1);
+        }
+        if (e < hi) {
+          const Rec<TI> c0 = W.z[e];
+          one(c0, dt[b], e);
+        }
       }
+    };
+    for (;;) {
+      run(cfA, cfB);
+      if (++r == tb.nruns) break;
+      run(cfB, cfA);
+      if (++r == tb.nruns) break;
     }
+    if (nb > 0) {
+      reduce(tb.n - nb, nb);
+      nb = 0;
+    }
+    // output rows of the chunk set's records (kept out of the run loop, whose
+    // waits count the coefficient loads in flight)
+    if (lane < tb.n) {
+      const TA* src = reinterpret_cast<const TA*>(&W.z[lane]);
+      const int info = W.mi[lane];
+      TA* o = dR + ((size_t)(i0 + ((info >> 20) & 7)) * nnei + (info & 0xfffff)) * 4;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) o[k] = src[k];
+    }
+    wave_sync();
   }
-  if (nb > 0) reduce_batch<TA, NLQ>(rl, nlq, blk, nb, dR, i0, nnei, lane);
 }
 
 bool dtype_ok(int dt) { return dt == DPC_F64 || dt == DPC_F32 || dt == DPC_F32_ACC64; }
@@ -597,7 +679,8 @@ int make_geo(int nloc, int ntypes, const int* sel, int m1, int m2, const dpc_ran
           r.d2 > 0 && r.L1 >= 1 && r.L2 >= 1 && r.offset >= 0))
       return DPC_ERANGE;
     const int64_t e = r.offset + (r.L1 + r.L2) * 6 * (int64_t)ld;
-    if (e * (int64_t)elem_bytes >= (int64_t(1) << 31)) return DPC_ENOTSUP;
+    // coefficient offsets must fit the key field; bytes must fit the buffer range
+    if (e > kOffMask || e * (int64_t)elem_bytes >= (int64_t(1) << 31)) return DPC_ENOTSUP;
     end = e > end ? e : end;
     PairRange& q = g->pr[p];
     q.lo = r.lo;
@@ -625,9 +708,10 @@ template <typename TI, typename TA>
 int launch_fwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype, const int* nlist,
                const void* em, void* T, void* D) {
   constexpr int NB = DPC_FWD_ATOMS_PER_WAVE;
+  static_assert(NB == 1 || NB == 2 || NB == 4 || NB == 8, "atoms per wave: 1, 2, 4 or 8");
   const dim3 grid((g.nloc + kWaves * NB - 1) / (kWaves * NB)), block(64 * kWaves);
-  const size_t shm =
-      (size_t)kWaves * NB * kChunk * sizeof(Rec) + (size_t)kWaves * g.m2 * 4 * sizeof(TA);
+  const size_t shm = kWaves * fwd_wave_bytes<TI, TA>(g.m2);
+  if (shm > kMaxLds) return DPC_ENOTSUP;
   (void)hipGetLastError();  // report only what this launch raises
   auto go = [&](auto kern) {
     hipLaunchKernelGGL(kern, grid, block, shm, s, g, (const TI*)coeff, atype, nlist,
@@ -645,13 +729,11 @@ template <typename TI, typename TA>
 int launch_bwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype, const int* nlist,
                const void* em, const void* dT, void* dR) {
   constexpr int NB = DPC_BWD_ATOMS_PER_WAVE;
+  static_assert(NB == 1 || NB == 2 || NB == 4 || NB == 8, "atoms per wave: 1, 2, 4 or 8");
   const dim3 grid((g.nloc + kWaves * NB - 1) / (kWaves * NB)), block(64 * kWaves);
   const int cpl = channels_per_lane(g.m1);
-  const int nl = (g.m1 + cpl - 1) / cpl;
-  const int blk = red_block_bytes((nl + 3) / 4);
-  const size_t wave_bytes = (size_t)NB * kChunk * sizeof(Rec) + 2 * kBatch * blk +
-                            16 * 4 * 2 * sizeof(TA) + kBatch * sizeof(int);
-  const size_t shm = kWaves * wave_bytes;
+  const size_t shm = kWaves * bwd_wave_bytes<TI>();
+  if (shm > kMaxLds) return DPC_ENOTSUP;
   (void)hipGetLastError();  // report only what this launch raises
   auto go = [&](auto kern) {
     hipLaunchKernelGGL(kern, grid, block, shm, s, g, (const TI*)coeff, atype, nlist,
