@@ -79,6 +79,19 @@ def cpu_baseline(x, seconds):
             "sample": f"atoms 0..{done - 1} of {n} ({pairs} valid pairs), fwd+bwd, {dt:.1f} s, {cpu}"}
 
 
+def copy_probe(mib):
+    """Device-to-device copy of `mib` MiB, three times (counter calibration)."""
+    import torch
+    n = mib * (1 << 20) // 8
+    a = torch.ones(n, dtype=torch.float64, device="cuda")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": n * 8, "launches": 3}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -88,12 +101,19 @@ def main():
     ap.add_argument("--dtype", default=None, choices=[None, "f64", "f32", "f32acc64"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run a plain device copy of this many MiB (3 times), the known-size "
+                         "kernel that calibrates the HBM byte counters, and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the descriptor kernel "
               "shards by atoms with no exchange, so multi-GPU throughput is not measured here.",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_probe_mib:
+        copy_probe(args.copy_probe_mib)
+        return
 
     import numpy as np
     import torch
