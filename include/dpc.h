@@ -123,7 +123,8 @@ int dpc_build_table(const dpc_net* net, const dpc_range* range, dpc_dtype dtype,
  *   atype    device int32 [nloc], values in [0, ntypes); an atom with another
  *            value gets NaN outputs (nothing is read out of bounds)
  *   nlist    device int32 [nloc][nnei]
- *   em       device R~ [nloc][nnei][4] (float64 for DPC_F64, else float32)
+ *   em       device R~ [nloc][nnei][4] (float64 for DPC_F64, else float32),
+ *            16-byte aligned (rows are read 16 bytes at a time)
  *   T        device out [nloc][m1][4]   (float32 only for DPC_F32)
  *   D        device out [nloc][m1][m2]  (float32 only for DPC_F32)
  * Requires 1 <= m1 <= DPC_MAX_M1, 1 <= m2 <= m1.  nloc = 0 is a no-op.      */
@@ -137,7 +138,7 @@ int dpc_se_a_tab_fwd(void* stream, dpc_dtype dtype, int nloc, int ntypes, const 
  *   w_m = sum_k' dE/dT_i[m][k'] R~_ij[k'],  x = R~_ij[0],
  * for valid j; padded rows are written as 0.
  *   dE_dT    device [nloc][m1][4] (float64 for DPC_F64, else float32)
- *   dE_dem   device out [nloc][nnei][4] (float32 only for DPC_F32)
+ *   dE_dem   device out [nloc][nnei][4] (float32 only for DPC_F32), 16-byte aligned
  * Other arguments as dpc_se_a_tab_fwd.                                      */
 int dpc_se_a_tab_bwd(void* stream, dpc_dtype dtype, int nloc, int ntypes, const int* sel,
                      int m1, const dpc_range* ranges, const void* coeff,

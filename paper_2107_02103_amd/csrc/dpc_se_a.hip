@@ -193,6 +193,7 @@ __device__ __forceinline__ void load_coef(__amdgpu_buffer_rsrc_t rs, int off, in
 // ---------------------------------------------------------------------------
 struct Tables {
   int n, nruns;                // records and runs of the chunk set
+  int rank;                    // this lane's slot: merged position, -1 padding, -2 no row
   int vs;                      // lane r: start of run r (n for r >= nruns)
   int vk;                      // lane r: key of run min(r, nruns - 1)
   int vp[2];                   // lane r: first record of atoms 1..NB-1 in run r, 8 bits each
@@ -204,30 +205,93 @@ __device__ __forceinline__ int split_at(const int (&p)[2], int b) {
   return (p[(b - 1) >> 2] >> (8 * ((b - 1) & 3))) & 255;
 }
 
+// Validity of the slots of one window: kWindow / NB slots per atom starting
+// at wbase, i.e. 32 slots per lane.  Bit k of lane l covers window index
+// l + 64 k = a * (kWindow / NB) + (j - wbase) (atom a, slot j).  Only the
+// sign of nlist is used, so one round trip to memory serves 32 chunk sets.
+constexpr int kWindow = 32 * kLanes;
+
+template <int NB>
+__device__ __forceinline__ uint32_t valid_window(const Geo& g, int i0, int wbase,
+                                                 const int* __restrict__ nlist, int lane) {
+  constexpr int W = kWindow / NB;
+  constexpr int kGroup = 8;   // loads in flight at once
+  uint32_t vm = 0;
+#pragma unroll 1
+  for (int k0 = 0; k0 < 32; k0 += kGroup) {
+    int v[kGroup];
+#pragma unroll
+    for (int q = 0; q < kGroup; ++q) {
+      const int il = lane + kLanes * (k0 + q);
+      const int a = il / W, j = wbase + il % W;
+      const bool in = i0 + a < g.nloc && j < g.nnei;
+      // out-of-range entries read slot 0 of atom i0 (always present) and are masked below
+      v[q] = __builtin_nontemporal_load(nlist + (in ? (size_t)(i0 + a) * g.nnei + j
+                                                    : (size_t)i0 * g.nnei));
+    }
+#pragma unroll
+    for (int q = 0; q < kGroup; ++q) {
+      const int il = lane + kLanes * (k0 + q);
+      const bool in = i0 + il / W < g.nloc && wbase + il % W < g.nnei;
+      vm |= (in && v[q] >= 0 ? 1u : 0u) << (k0 + q);
+    }
+  }
+  return vm;
+}
+
+// One R~ row (16-byte aligned: checked on the host).
+template <typename TI>
+__device__ __forceinline__ void load_row(const TI* p, TI (&r)[4]) {
+  if constexpr (sizeof(TI) == 8) {
+    typedef TI V2 __attribute__((ext_vector_type(2)));
+    const V2 a = __builtin_nontemporal_load(reinterpret_cast<const V2*>(p));
+    const V2 b = __builtin_nontemporal_load(reinterpret_cast<const V2*>(p) + 1);
+    r[0] = a.x; r[1] = a.y; r[2] = b.x; r[3] = b.y;
+  } else {
+    typedef TI V4 __attribute__((ext_vector_type(4)));
+    const V4 a = __builtin_nontemporal_load(reinterpret_cast<const V4*>(p));
+    r[0] = a.x; r[1] = a.y; r[2] = a.z; r[3] = a.w;
+  }
+}
+
+// One dE/dR~ row (16-byte aligned: checked on the host).
+template <typename TA>
+__device__ __forceinline__ void store_row(TA* p, const TA (&v)[4]) {
+  if constexpr (sizeof(TA) == 8) {
+    typedef TA V2 __attribute__((ext_vector_type(2)));
+    __builtin_nontemporal_store(V2{v[0], v[1]}, reinterpret_cast<V2*>(p));
+    __builtin_nontemporal_store(V2{v[2], v[3]}, reinterpret_cast<V2*>(p) + 1);
+  } else {
+    typedef TA V4 __attribute__((ext_vector_type(4)));
+    __builtin_nontemporal_store(V4{v[0], v[1], v[2], v[3]}, reinterpret_cast<V4*>(p));
+  }
+}
+
 // Merge slots [s0, s0 + 64/NB) of the wave's NB atoms into W and build the
-// run tables.  In the backward pass (kBwd) padded slots get a zero output row
-// and clamped records a zero R~ row.
+// run tables.  Lane l covers slot s0 + l % (64/NB) of atom l / (64/NB).  In
+// the backward pass (kBwd) clamped records get a zero R~ row.
 template <typename TI, typename TA, int NB, bool kBwd>
 __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[NB], int i0,
-                                                  int s0, const int* __restrict__ nlist,
+                                                  int s0, int wbase, uint32_t vm,
                                                   const TI* __restrict__ em, WaveLds<TI>& W,
-                                                  TA* __restrict__ dR, int lane) {
+                                                  int lane) {
   constexpr int kC = kLanes / NB;
   const int a = lane / kC, sl = lane % kC, j = s0 + sl;
   int at = -1;
 #pragma unroll
   for (int b = 0; b < NB; ++b)
     if (b == a) at = ai[b];
+  // the lane of the window masks that holds this slot's bit
+  const int il = a * (kWindow / NB) + (s0 - wbase) + sl;
+  const int holder = __builtin_amdgcn_ds_bpermute((il & 63) << 2, (int)vm);
   bool valid = false;
   Rec<TI> rec;
   int key = 0;
   if (at >= 0 && j < g.nnei) {
     const size_t row = (size_t)(i0 + a) * g.nnei + j;
-    valid = nlist[row] >= 0;
+    valid = (holder >> (il >> 6)) & 1;
     if (valid) {
-      const TI* e = em + row * 4;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) rec.r[k] = e[k];
+      load_row(em + row * 4, rec.r);
       const int blk = block_of(g, j);
       const PairRange& P = g.pr[at * g.ntypes + blk];
       int l;
@@ -239,13 +303,11 @@ __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[
 #pragma unroll
         for (int k = 0; k < 4; ++k) rec.r[k] = (TI)0;
       }
-    } else if constexpr (kBwd) {
-      TA* o = dR + row * 4;
-      o[0] = o[1] = o[2] = o[3] = (TA)0;
     }
   }
+  const int has_row = at >= 0 && j < g.nnei;
   const uint64_t m = __ballot(valid);
-  if (m == 0) return Tables{0, 0, 0, 0, {0, 0}};
+  if (m == 0) return Tables{0, 0, has_row ? -1 : -2, 0, 0, {0, 0}};
   const uint64_t seg = kC == 64 ? ~0ull : ((1ull << kC) - 1);
   const uint64_t before_seg = a == 0 ? 0ull : ((1ull << (a * kC)) - 1);
   const int pos = lanes_below(m) - __popcll(m & before_seg);
@@ -288,6 +350,7 @@ __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[
   wave_sync();
 
   Tables T;
+  T.rank = valid ? r : (has_row ? -1 : -2);
   T.n = __popcll(m);
   const bool in = lane < T.n;
   const int ke = W.mk[lane], ae = (W.mi[lane] >> 20) & 7;
@@ -321,13 +384,21 @@ __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[
 // ---------------------------------------------------------------------------
 // forward: T and D
 // ---------------------------------------------------------------------------
+// The epilogue reuses the chunk-set LDS of the wave for the atom's T rows.
 template <typename TI, typename TA>
-__host__ __device__ constexpr size_t fwd_wave_bytes(int m2) {
-  return align16(sizeof(WaveLds<TI>)) + align16((size_t)m2 * 4 * sizeof(TA));
+__host__ __device__ constexpr size_t fwd_wave_bytes(int m1) {
+  return align16(sizeof(WaveLds<TI>)) > align16((size_t)m1 * 4 * sizeof(TA))
+             ? align16(sizeof(WaveLds<TI>))
+             : align16((size_t)m1 * 4 * sizeof(TA));
 }
 
+template <typename TA>
+using Pair = TA __attribute__((ext_vector_type(2)));
+
 template <typename TI, typename TA, int CPL, int NB>
-__global__ __launch_bounds__(64 * kWaves) void se_a_fwd_kernel(
+// up to 128 channels: registers capped so that 3 wavefronts fit on a SIMD
+__global__ __launch_bounds__(64 * kWaves)
+__attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_fwd_kernel(
     const Geo g, const TI* __restrict__ coeff, const int* __restrict__ atype,
     const int* __restrict__ nlist, const TI* __restrict__ em, TA* __restrict__ T,
     TA* __restrict__ D) {
@@ -338,9 +409,8 @@ __global__ __launch_bounds__(64 * kWaves) void se_a_fwd_kernel(
   const int i0 = __builtin_amdgcn_readfirstlane((blockIdx.x * kWaves + wave) * NB);
   if (i0 >= g.nloc) return;
   const int nnei = g.nnei, m1 = g.m1, m2 = g.m2, ld = g.ld;
-  unsigned char* wb = smem + wave * fwd_wave_bytes<TI, TA>(m2);
+  unsigned char* wb = smem + wave * fwd_wave_bytes<TI, TA>(m1);
   WaveLds<TI>& W = *reinterpret_cast<WaveLds<TI>*>(wb);
-  TA* sT = reinterpret_cast<TA*>(wb + align16(sizeof(WaveLds<TI>)));
   const __amdgpu_buffer_rsrc_t rs = make_rsrc(coeff, g.coeff_bytes);
   const int voff = min(lane * CPL, ld - CPL) * (int)sizeof(TI);
 
@@ -371,9 +441,18 @@ __global__ __launch_bounds__(64 * kWaves) void se_a_fwd_kernel(
   }
   TI cfA[6][CPL], cfB[6][CPL];
 
-  for (int s0 = 0; s0 < nnei; s0 += kC) {
-    const Tables tb = build_chunk_set<TI, TA, NB, false>(g, ai, i0, s0, nlist, em, W,
-                                                         (TA*)nullptr, lane);
+  // Chunk sets are visited cyclically from a start that differs between
+  // wavefronts, so that waves sharing a SIMD are not all building (a
+  // latency-bound phase) at the same time.
+  const int nch = (nnei + kC - 1) / kC;
+  int s0 = ((int)(blockIdx.x * 5 + wave * 3) % nch) * kC;
+  uint32_t vm = 0;
+  for (int cc = 0, wbase = -1; cc < nch; ++cc, s0 = s0 + kC < nnei ? s0 + kC : 0) {
+    if (s0 - s0 % (kWindow / NB) != wbase) {  // window of nlist signs holding s0
+      wbase = s0 - s0 % (kWindow / NB);
+      vm = valid_window<NB>(g, i0, wbase, nlist, lane);
+    }
+    const Tables tb = build_chunk_set<TI, TA, NB, false>(g, ai, i0, s0, wbase, vm, em, W, lane);
     if (tb.n == 0) continue;
     load_coef<TI, CPL>(rs, key_offset(readlane(tb.vk, 0)), ld, voff, cfA);
     int r = 0;
@@ -425,40 +504,50 @@ __global__ __launch_bounds__(64 * kWaves) void se_a_fwd_kernel(
     wave_sync();
   }
 
-  // T rows and D = T (T<)^T of each atom
+  // T and D = T (T<)^T of each atom.  The rows go through LDS so that both
+  // outputs are written in flat order, consecutive lanes to consecutive
+  // addresses; lane f of a D pass computes element f = m * m2 + n.
+  TA* sT = reinterpret_cast<TA*>(wb);
+  const int m_step = 64 / m2, n_step = 64 % m2;
 #pragma unroll
   for (int a = 0; a < NB; ++a) {
     const int i = i0 + a;
     if (ai[a] < 0) continue;
-#pragma unroll
-    for (int h = 0; h < CPL; ++h) {
-      const int m = lane * CPL + h;
-      if (m < m1) {
-        TA* Tm = T + ((size_t)i * m1 + m) * 4;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) Tm[k] = acc[a][h][k];
-      }
-      if (m < m2) {
-#pragma unroll
-        for (int k = 0; k < 4; ++k) sT[m * 4 + k] = acc[a][h][k];
-      }
-    }
     wave_sync();
 #pragma unroll
     for (int h = 0; h < CPL; ++h) {
       const int m = lane * CPL + h;
       if (m < m1) {
-        TA* Dm = D + ((size_t)i * m1 + m) * m2;
-        for (int n = 0; n < m2; ++n) {
-          TA v = acc[a][h][0] * sT[n * 4 + 0];
-          v = fma(acc[a][h][1], sT[n * 4 + 1], v);
-          v = fma(acc[a][h][2], sT[n * 4 + 2], v);
-          v = fma(acc[a][h][3], sT[n * 4 + 3], v);
-          Dm[n] = v;
-        }
+        Pair<TA>* d = reinterpret_cast<Pair<TA>*>(sT + m * 4);
+        d[0] = Pair<TA>{acc[a][h][0], acc[a][h][1]};
+        d[1] = Pair<TA>{acc[a][h][2], acc[a][h][3]};
       }
     }
     wave_sync();
+    TA* Ti = T + (size_t)i * m1 * 4;
+    for (int e = lane; e < m1 * 2; e += 64) {
+      const Pair<TA> v = reinterpret_cast<const Pair<TA>*>(sT)[e];
+      __builtin_nontemporal_store(v.x, Ti + 2 * e);
+      __builtin_nontemporal_store(v.y, Ti + 2 * e + 1);
+    }
+    TA* Di = D + (size_t)i * m1 * m2;
+    int m = lane / m2, n = lane % m2;
+    for (int f = lane; f < m1 * m2; f += 64) {
+      const Pair<TA>* pm = reinterpret_cast<const Pair<TA>*>(sT + m * 4);
+      const Pair<TA>* pn = reinterpret_cast<const Pair<TA>*>(sT + n * 4);
+      const Pair<TA> a0 = pm[0], a1 = pm[1], b0 = pn[0], b1 = pn[1];
+      TA v = a0.x * b0.x;
+      v = fma(a0.y, b0.y, v);
+      v = fma(a1.x, b1.x, v);
+      v = fma(a1.y, b1.y, v);
+      __builtin_nontemporal_store(v, Di + f);
+      m += m_step;
+      n += n_step;
+      if (n >= m2) {
+        n -= m2;
+        ++m;
+      }
+    }
   }
 }
 
@@ -485,11 +574,10 @@ __host__ __device__ constexpr size_t bwd_wave_bytes() {
   return align16(sizeof(WaveLds<TI>)) + (size_t)2 * kBatch * kRedBlock;
 }
 
-template <typename TA>
-using Pair = TA __attribute__((ext_vector_type(2)));
-
 template <typename TI, typename TA, int CPL, int NB>
-__global__ __launch_bounds__(64 * kWaves) void se_a_bwd_kernel(
+// up to 128 channels: registers capped so that 3 wavefronts fit on a SIMD
+__global__ __launch_bounds__(64 * kWaves)
+__attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
     const Geo g, const TI* __restrict__ coeff, const int* __restrict__ atype,
     const int* __restrict__ nlist, const TI* __restrict__ em, const TI* __restrict__ dT,
     TA* __restrict__ dR) {
@@ -523,7 +611,9 @@ __global__ __launch_bounds__(64 * kWaves) void se_a_bwd_kernel(
       const int m = lane * CPL + h;
 #pragma unroll
       for (int k = 0; k < 4; ++k)
-        dt[a][h][k] = (i < g.nloc && m < m1) ? (TA)dT[((size_t)i * m1 + m) * 4 + k] : (TA)0;
+        dt[a][h][k] = (i < g.nloc && m < m1)
+                          ? (TA)__builtin_nontemporal_load(dT + ((size_t)i * m1 + m) * 4 + k)
+                          : (TA)0;
     }
     if (i < g.nloc) {
       const int t = __builtin_amdgcn_readfirstlane(atype[i]);
@@ -561,9 +651,36 @@ __global__ __launch_bounds__(64 * kWaves) void se_a_bwd_kernel(
   };
   static_assert(4 * sizeof(TA) <= sizeof(Rec<TI>), "a record slot holds one output row");
 
-  for (int s0 = 0; s0 < nnei; s0 += kC) {
-    const Tables tb = build_chunk_set<TI, TA, NB, true>(g, ai, i0, s0, nlist, em, W, dR, lane);
-    if (tb.n == 0) continue;
+  // Chunk sets are visited cyclically from a start that differs between
+  // wavefronts, so that waves sharing a SIMD are not all building (a
+  // latency-bound phase) at the same time.
+  const int nch = (nnei + kC - 1) / kC;
+  int s0 = ((int)(blockIdx.x * 5 + wave * 3) % nch) * kC;
+  uint32_t vm = 0;
+  for (int cc = 0, wbase = -1; cc < nch; ++cc, s0 = s0 + kC < nnei ? s0 + kC : 0) {
+    if (s0 - s0 % (kWindow / NB) != wbase) {  // window of nlist signs holding s0
+      wbase = s0 - s0 % (kWindow / NB);
+      vm = valid_window<NB>(g, i0, wbase, nlist, lane);
+    }
+    const Tables tb = build_chunk_set<TI, TA, NB, true>(g, ai, i0, s0, wbase, vm, em, W, lane);
+    // Each lane writes the dE/dR~ row of its own slot (zero for padding) after
+    // the chunk set's runs: consecutive lanes, consecutive rows, and no store
+    // ahead of the coefficient loads whose waits would then include it.
+    auto write_rows = [&]() __attribute__((always_inline)) {
+      if (tb.rank >= -1) {
+        TA v[4] = {(TA)0, (TA)0, (TA)0, (TA)0};
+        if (tb.rank >= 0) {
+          const TA* src = reinterpret_cast<const TA*>(&W.z[tb.rank]);
+#pragma unroll
+          for (int k = 0; k < 4; ++k) v[k] = src[k];
+        }
+        store_row(dR + ((size_t)(i0 + lane / kC) * nnei + s0 + lane % kC) * 4, v);
+      }
+    };
+    if (tb.n == 0) {
+      write_rows();
+      continue;
+    }
     load_coef<TI, CPL>(rs, key_offset(readlane(tb.vk, 0)), ld, voff, cfA);
     int r = 0;
     auto run = [&](TI (&cur)[6][CPL], TI (&nxt)[6][CPL]) __attribute__((always_inline)) {
@@ -633,15 +750,8 @@ __global__ __launch_bounds__(64 * kWaves) void se_a_bwd_kernel(
       reduce(tb.n - nb, nb);
       nb = 0;
     }
-    // output rows of the chunk set's records (kept out of the run loop, whose
-    // waits count the coefficient loads in flight)
-    if (lane < tb.n) {
-      const TA* src = reinterpret_cast<const TA*>(&W.z[lane]);
-      const int info = W.mi[lane];
-      TA* o = dR + ((size_t)(i0 + ((info >> 20) & 7)) * nnei + (info & 0xfffff)) * 4;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) o[k] = src[k];
-    }
+    wave_sync();
+    write_rows();
     wave_sync();
   }
 }
@@ -710,7 +820,7 @@ int launch_fwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
   constexpr int NB = DPC_FWD_ATOMS_PER_WAVE;
   static_assert(NB == 1 || NB == 2 || NB == 4 || NB == 8, "atoms per wave: 1, 2, 4 or 8");
   const dim3 grid((g.nloc + kWaves * NB - 1) / (kWaves * NB)), block(64 * kWaves);
-  const size_t shm = kWaves * fwd_wave_bytes<TI, TA>(g.m2);
+  const size_t shm = kWaves * fwd_wave_bytes<TI, TA>(g.m1);
   if (shm > kMaxLds) return DPC_ENOTSUP;
   (void)hipGetLastError();  // report only what this launch raises
   auto go = [&](auto kern) {
@@ -761,6 +871,7 @@ extern "C" int dpc_se_a_tab_fwd(void* stream, dpc_dtype dtype, int nloc, int nty
   if (st != DPC_OK) return st;
   if (nloc == 0) return DPC_OK;
   if (!coeff || !atype || !nlist || !em || !T || !D) return DPC_EINVAL;
+  if (reinterpret_cast<uintptr_t>(em) % 16) return DPC_EINVAL;  // rows are read 16 bytes at a time
   hipStream_t s = static_cast<hipStream_t>(stream);
   switch (dtype) {
     case DPC_F64: return launch_fwd<double, double>(s, g, coeff, atype, nlist, em, T, D);
@@ -779,6 +890,9 @@ extern "C" int dpc_se_a_tab_bwd(void* stream, dpc_dtype dtype, int nloc, int nty
   if (st != DPC_OK) return st;
   if (nloc == 0) return DPC_OK;
   if (!coeff || !atype || !nlist || !em || !dE_dT || !dE_dem) return DPC_EINVAL;
+  // rows are read and written 16 bytes at a time
+  if (reinterpret_cast<uintptr_t>(em) % 16 || reinterpret_cast<uintptr_t>(dE_dem) % 16)
+    return DPC_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
   switch (dtype) {
     case DPC_F64: return launch_bwd<double, double>(s, g, coeff, atype, nlist, em, dE_dT, dE_dem);

@@ -138,6 +138,7 @@ def test_kernel_entry_points_validate_before_launch():
         (dict(ntypes=9, sel=[1] * 9), B.DPC_ENOTSUP), (dict(m1=300, m2=4), B.DPC_ENOTSUP),
         (dict(nloc=-1), B.DPC_EINVAL), (dict(sel=[4, -1]), B.DPC_EINVAL),
         (dict(em=0), B.DPC_EINVAL), (dict(T=0), B.DPC_EINVAL),
+        (dict(em=fake + 8), B.DPC_EINVAL),                         # R~ not 16-byte aligned
     ]
     for kw, code in cases:
         a = dict(stream=0, dtype=P.DPC_F64, nloc=3, ntypes=2, sel=sel, m1=8, m2=4, ranges=r,
@@ -152,6 +153,12 @@ def test_kernel_entry_points_validate_before_launch():
     with pytest.raises(P.DpcError) as e:
         P.dpc_se_a_tab_bwd(0, P.DPC_F64, 3, 2, sel, 8, bad, fake, fake, fake, fake, fake, fake)
     assert e.value.status == B.DPC_ERANGE
+    with pytest.raises(P.DpcError) as e:
+        P.dpc_se_a_tab_bwd(0, P.DPC_F64, 3, 2, sel, 8, r, fake, fake, fake, fake + 8, fake, fake)
+    assert e.value.status == B.DPC_EINVAL
+    with pytest.raises(P.DpcError) as e:                              # dE/dR~ not 16-byte aligned
+        P.dpc_se_a_tab_bwd(0, P.DPC_F64, 3, 2, sel, 8, r, fake, fake, fake, fake, fake, fake + 8)
+    assert e.value.status == B.DPC_EINVAL
     # nloc = 0 is a no-op that launches nothing
     P.dpc_se_a_tab_fwd(0, P.DPC_F64, 0, 2, sel, 8, 4, r, 0, 0, 0, 0, 0, 0)
     P.dpc_se_a_tab_bwd(0, P.DPC_F64, 0, 2, sel, 8, r, 0, 0, 0, 0, 0, 0)
