@@ -68,6 +68,7 @@ struct PairRange {             // one ordered type pair's table, as the kernels 
 struct Geo {
   int nloc, nnei, ntypes, m1, m2, ld;
   int coeff_bytes;             // size of the coefficient buffer (bounds the buffer loads)
+  int pair_out;                // forward: T and D may be written 16 bytes at a time
   int blk_end[DPC_MAX_TYPES];  // slot index one past the end of each sel block
   PairRange pr[DPC_MAX_TYPES * DPC_MAX_TYPES];
 };
@@ -525,27 +526,49 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_fwd_kernel(
     }
     wave_sync();
     TA* Ti = T + (size_t)i * m1 * 4;
-    for (int e = lane; e < m1 * 2; e += 64) {
-      const Pair<TA> v = reinterpret_cast<const Pair<TA>*>(sT)[e];
-      __builtin_nontemporal_store(v.x, Ti + 2 * e);
-      __builtin_nontemporal_store(v.y, Ti + 2 * e + 1);
-    }
     TA* Di = D + (size_t)i * m1 * m2;
-    int m = lane / m2, n = lane % m2;
-    for (int f = lane; f < m1 * m2; f += 64) {
+    auto dot = [&](int m, int n) __attribute__((always_inline)) -> TA {
       const Pair<TA>* pm = reinterpret_cast<const Pair<TA>*>(sT + m * 4);
       const Pair<TA>* pn = reinterpret_cast<const Pair<TA>*>(sT + n * 4);
       const Pair<TA> a0 = pm[0], a1 = pm[1], b0 = pn[0], b1 = pn[1];
       TA v = a0.x * b0.x;
       v = fma(a0.y, b0.y, v);
       v = fma(a1.x, b1.x, v);
-      v = fma(a1.y, b1.y, v);
-      __builtin_nontemporal_store(v, Di + f);
-      m += m_step;
-      n += n_step;
-      if (n >= m2) {
-        n -= m2;
-        ++m;
+      return (TA)fma(a1.y, b1.y, v);
+    };
+    if (g.pair_out) {
+      // two elements per lane and store
+      for (int e = lane; e < m1 * 2; e += 64)
+        __builtin_nontemporal_store(reinterpret_cast<const Pair<TA>*>(sT)[e],
+                                    reinterpret_cast<Pair<TA>*>(Ti) + e);
+      const int ms = 128 / m2, ns = 128 % m2;
+      int m = (2 * lane) / m2, n = (2 * lane) % m2;
+      for (int f2 = lane; f2 < m1 * m2 / 2; f2 += 64) {
+        int mb = m, nb = n + 1;
+        if (nb == m2) {
+          nb = 0;
+          ++mb;
+        }
+        __builtin_nontemporal_store(Pair<TA>{dot(m, n), dot(mb, nb)},
+                                    reinterpret_cast<Pair<TA>*>(Di) + f2);
+        m += ms;
+        n += ns;
+        if (n >= m2) {
+          n -= m2;
+          ++m;
+        }
+      }
+    } else {
+      for (int e = lane; e < m1 * 4; e += 64) __builtin_nontemporal_store(sT[e], Ti + e);
+      int m = lane / m2, n = lane % m2;
+      for (int f = lane; f < m1 * m2; f += 64) {
+        __builtin_nontemporal_store(dot(m, n), Di + f);
+        m += m_step;
+        n += n_step;
+        if (n >= m2) {
+          n -= m2;
+          ++m;
+        }
       }
     }
   }
@@ -808,6 +831,7 @@ int make_geo(int nloc, int ntypes, const int* sel, int m1, int m2, const dpc_ran
   g->m2 = m2;
   g->ld = ld;
   g->coeff_bytes = (int)(end * (int64_t)elem_bytes);
+  g->pair_out = 0;
   return DPC_OK;
 }
 
@@ -872,6 +896,8 @@ extern "C" int dpc_se_a_tab_fwd(void* stream, dpc_dtype dtype, int nloc, int nty
   if (nloc == 0) return DPC_OK;
   if (!coeff || !atype || !nlist || !em || !T || !D) return DPC_EINVAL;
   if (reinterpret_cast<uintptr_t>(em) % 16) return DPC_EINVAL;  // rows are read 16 bytes at a time
+  g.pair_out = reinterpret_cast<uintptr_t>(T) % 16 == 0 && reinterpret_cast<uintptr_t>(D) % 16 == 0 &&
+               (m1 * m2) % 2 == 0;
   hipStream_t s = static_cast<hipStream_t>(stream);
   switch (dtype) {
     case DPC_F64: return launch_fwd<double, double>(s, g, coeff, atype, nlist, em, T, D);
