@@ -74,7 +74,7 @@ struct Geo {
 };
 
 template <typename TI>
-struct Rec {                   // one valid neighbour, as staged in LDS
+struct alignas(16) Rec {       // one valid neighbour, as staged in LDS
   TI r[4];                     // its row of R~ (zero in the backward pass when clamped)
   double t;                    // offset from the left node of its interval
   double pad;
@@ -91,6 +91,15 @@ struct WaveLds {
 };
 
 __host__ __device__ constexpr size_t align16(size_t x) { return (x + 15) & ~size_t(15); }
+
+// Record e of a wave's merged list, the list starting `zoff` bytes into the
+// workgroup's LDS.  The offset is formed in 32 bits (indexing through a
+// generic pointer costs a 64-bit multiply-add per read).
+template <typename TI>
+__device__ __forceinline__ const Rec<TI>& zrec(const unsigned char* lds, uint32_t zoff, int e) {
+  return *reinterpret_cast<const Rec<TI>*>(
+      __builtin_assume_aligned(lds + zoff + (uint32_t)e * (uint32_t)sizeof(Rec<TI>), 16));
+}
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v2i __attribute__((ext_vector_type(2)));
@@ -410,7 +419,8 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_fwd_kernel(
   const int i0 = __builtin_amdgcn_readfirstlane((blockIdx.x * kWaves + wave) * NB);
   if (i0 >= g.nloc) return;
   const int nnei = g.nnei, m1 = g.m1, m2 = g.m2, ld = g.ld;
-  unsigned char* wb = smem + wave * fwd_wave_bytes<TI, TA>(m1);
+  const uint32_t zoff = __builtin_amdgcn_readfirstlane(wave * (uint32_t)fwd_wave_bytes<TI, TA>(m1));
+  unsigned char* wb = smem + zoff;
   WaveLds<TI>& W = *reinterpret_cast<WaveLds<TI>*>(wb);
   const __amdgpu_buffer_rsrc_t rs = make_rsrc(coeff, g.coeff_bytes);
   const int voff = min(lane * CPL, ld - CPL) * (int)sizeof(TI);
@@ -486,12 +496,12 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_fwd_kernel(
         const int hi = b == NB - 1 ? E : split_at<NB>(p, b + 1);
         int e = lo;
         for (; e + 1 < hi; e += 2) {
-          const Rec<TI> c0 = W.z[e], c1 = W.z[e + 1];
+          const Rec<TI> c0 = zrec<TI>(smem, zoff, e), c1 = zrec<TI>(smem, zoff, e + 1);
           one(c0, acc[b]);
           one(c1, acc[b]);
         }
         if (e < hi) {
-          const Rec<TI> c0 = W.z[e];
+          const Rec<TI> c0 = zrec<TI>(smem, zoff, e);
           one(c0, acc[b]);
         }
       }
@@ -613,7 +623,8 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
   if (i0 >= g.nloc) return;
   const int nnei = g.nnei, m1 = g.m1, ld = g.ld;
   static_assert(16 * part_stride<TA>() * sizeof(TA) <= 2 * kBatch * kRedBlock, "step 2 rows");
-  unsigned char* wb = smem + wave * bwd_wave_bytes<TI>();
+  const uint32_t zoff = __builtin_amdgcn_readfirstlane(wave * (uint32_t)bwd_wave_bytes<TI>());
+  unsigned char* wb = smem + zoff;
   WaveLds<TI>& W = *reinterpret_cast<WaveLds<TI>*>(wb);
   unsigned char* red = wb + align16(sizeof(WaveLds<TI>));
   TA* part = reinterpret_cast<TA*>(red);
@@ -753,12 +764,12 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
         const int hi = b == NB - 1 ? E : split_at<NB>(p, b + 1);
         int e = lo;
         for (; e + 1 < hi; e += 2) {
-          const Rec<TI> c0 = W.z[e], c1 = W.z[e + 1];
+          const Rec<TI> c0 = zrec<TI>(smem, zoff, e), c1 = zrec<TI>(smem, zoff, e + 1);
           one(c0, dt[b], e);
           one(c1, dt[b], e + 1);
         }
         if (e < hi) {
-          const Rec<TI> c0 = W.z[e];
+          const Rec<TI> c0 = zrec<TI>(smem, zoff, e);
           one(c0, dt[b], e);
         }
       }
