@@ -279,12 +279,15 @@ __device__ __forceinline__ void store_row(TA* p, const TA (&v)[4]) {
 
 // Merge slots [s0, s0 + 64/NB) of the wave's NB atoms into W and build the
 // run tables.  Lane l covers slot s0 + l % (64/NB) of atom l / (64/NB).  In
-// the backward pass (kBwd) clamped records get a zero R~ row.
-template <typename TI, typename TA, int NB, bool kBwd>
+// the backward pass (kBwd) clamped records get a zero R~ row.  With kPairs
+// the lane also gets the index of its record's (interval, atom) pair among
+// the chunk set's pairs in merged order (`pair`, -1 without a record), a
+// pair being a maximal group of records with equal key and atom.
+template <typename TI, typename TA, int NB, bool kBwd, bool kPairs = false>
 __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[NB], int i0,
                                                   int s0, int wbase, uint32_t vm,
                                                   const TI* __restrict__ em, WaveLds<TI>& W,
-                                                  int lane) {
+                                                  int lane, int* pair = nullptr) {
   constexpr int kC = kLanes / NB;
   const int a = lane / kC, sl = lane % kC, j = s0 + sl;
   int at = -1;
@@ -317,6 +320,7 @@ __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[
   }
   const int has_row = at >= 0 && j < g.nnei;
   const uint64_t m = __ballot(valid);
+  if constexpr (kPairs) *pair = -1;
   if (m == 0) return Tables{0, 0, has_row ? -1 : -2, 0, 0, {0, 0}};
   const uint64_t seg = kC == 64 ? ~0ull : ((1ull << kC) - 1);
   const uint64_t before_seg = a == 0 ? 0ull : ((1ull << (a * kC)) - 1);
@@ -374,7 +378,14 @@ __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[
     W.rs[rr] = lane;
   }
   if (lane == 0) W.rs[T.nruns] = T.n;
+  if constexpr (kPairs) {
+    const int ap = (W.mi[lane > 0 ? lane - 1 : 0] >> 20) & 7;
+    const uint64_t F2 = __ballot(in && (lane == 0 || ke != kp || ae != ap));
+    wave_sync();              // every lane has read mk: it now takes the pair indices
+    W.mk[lane] = lanes_below(F2) + (int)((F2 >> lane) & 1) - 1;
+  }
   wave_sync();
+  if constexpr (kPairs) *pair = valid ? W.mk[r] : -1;
   const int S = W.rs[min(lane, T.nruns)], E = W.rs[min(lane + 1, T.nruns)];
   T.vs = S;
   T.vk = W.rk[min(lane, max(T.nruns - 1, 0))];
@@ -790,6 +801,223 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// backward, float64, M1 <= 112: channel sums on the matrix cores
+// ---------------------------------------------------------------------------
+// For one interval (coefficients C[m][q], g_m(t) = sum_q C[m][q] t^q) and
+// one atom (dE/dT rows dT[m][k]) both channel sums of a record factor
+// through the 4 x 6 matrix P[k][q] = sum_m dT[m][k] C[m][q]:
+//   sum_m dT[m][k] g_m(t)                  = sum_q t^q P[k][q]
+//   sum_m g'_m(t) sum_k' dT[m][k'] R~[k']  = sum_k' R~[k'] sum_q q t^(q-1) P[k'][q].
+// P of each (interval, atom) pair of a chunk set is one chain of
+// v_mfma_f64_4x4x4f64, and each record then costs a few dozen operations in
+// the lane that owns its slot.
+//
+// v_mfma_f64_4x4x4f64 computes four independent 4x4 products D_b = A_b B_b
+// (+ C_b).  Lane L = 16 kk + 4 b + x holds A_b[x][kk] and B_b[kk][x]; D_b[i][j]
+// sits in lane 16 i + 4 b + j (measured on gfx950).  Here block b = 2 h + g:
+// g selects the powers 4g .. 4g+3 (6 and 7 are not used), h the half of the
+// channels, 4S channels each.  K step s < 2 (S / 2) of half h covers the
+// channels h*4S + 8(s/2) + 2kk + s%2, so that one 16-byte load of a lane
+// brings its coefficients for two consecutive K steps; for odd S the last
+// step covers h*4S + 4(S-1) + kk.  The two halves' products are summed when a
+// record reads P.
+constexpr int kPairSlots = 16;     // (interval, atom) products held in LDS at once
+
+__host__ __device__ constexpr size_t bwdm_wave_bytes() {
+  return align16(sizeof(WaveLds<double>)) + (size_t)kPairSlots * 64 * sizeof(double);
+}
+
+__device__ __forceinline__ double mfma4(double a, double b, double c) {
+  return __builtin_amdgcn_mfma_f64_4x4x4f64(a, b, c, 0, 0, 0);
+}
+
+constexpr int kMfmaAtoms = 4;      // atoms per wavefront in the matrix-core kernel
+
+// 4 atoms' dE/dT operands and two coefficient sets take more than 168
+// registers: two wavefronts per SIMD
+template <int S>
+__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2)))
+void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
+                          const int* __restrict__ atype, const int* __restrict__ nlist,
+                          const double* __restrict__ em, const double* __restrict__ dT,
+                          double* __restrict__ dR) {
+  static_assert(S >= 1 && S <= 14, "K steps per channel half");
+  constexpr int S2 = S / 2;           // 16-byte loads per interval
+  constexpr int kLoads = S2 + S % 2;  // loads per interval
+  extern __shared__ __align__(16) unsigned char smem[];
+  constexpr int NB = kMfmaAtoms;
+  constexpr int kC = kLanes / NB;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int i0 = __builtin_amdgcn_readfirstlane((blockIdx.x * kWaves + wave) * NB);
+  if (i0 >= g.nloc) return;
+  const int nnei = g.nnei, m1 = g.m1, ld = g.ld;
+  const uint32_t zoff = __builtin_amdgcn_readfirstlane(wave * (uint32_t)bwdm_wave_bytes());
+  unsigned char* wb = smem + zoff;
+  WaveLds<double>& W = *reinterpret_cast<WaveLds<double>*>(wb);
+  double* const store = reinterpret_cast<double*>(wb + align16(sizeof(WaveLds<double>)));
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(coeff, g.coeff_bytes);
+
+  // this lane's place in the MFMA operands
+  const int kk = lane >> 4, h = (lane >> 3) & 1, x = lane & 3;
+  const int q = min(4 * ((lane >> 2) & 1) + x, 5);   // power held in B (6, 7 repeat 5)
+  const int ch0 = h * 4 * S + 2 * kk;                 // channel of K step 0
+  const int boff = (q * ld + ch0) * (int)sizeof(double);
+  const int boff_last = (q * ld + h * 4 * S + 4 * (S - 1) + kk) * (int)sizeof(double);
+  auto channel = [&](int s) __attribute__((always_inline)) {
+    return s < 2 * S2 ? ch0 + 8 * (s >> 1) + (s & 1) : h * 4 * S + 4 * (S - 1) + kk;
+  };
+
+  // A operands: dT of the wave's atoms, transposed, zero past M1
+  double A[NB][S];
+  int ai[NB];
+#pragma unroll
+  for (int a = 0; a < NB; ++a) {
+    const int i = i0 + a;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      const int m = channel(s);
+      A[a][s] = (i < g.nloc && m < m1)
+                    ? __builtin_nontemporal_load(dT + ((size_t)i * m1 + m) * 4 + x)
+                    : 0.0;
+    }
+    ai[a] = -1;
+    if (i < g.nloc) {
+      const int t = __builtin_amdgcn_readfirstlane(atype[i]);
+      if (t < 0 || t >= g.ntypes) {  // invalid type: the atom's outputs become NaN
+        for (int e = lane; e < nnei * 4; e += 64) dR[(size_t)i * nnei * 4 + e] = (double)NAN;
+      } else {
+        ai[a] = t;
+      }
+    }
+  }
+
+  // B operands of one interval: coefficients at element offset `off`
+  auto load_b = [&](int off, double (&B)[S]) __attribute__((always_inline)) {
+    const int soff = off * (int)sizeof(double);
+#pragma unroll
+    for (int s2 = 0; s2 < S2; ++s2) {
+      const v4i v = __builtin_amdgcn_raw_buffer_load_b128(rs, boff, soff + 64 * s2, 0);
+      double p[2];
+      __builtin_memcpy(p, &v, sizeof(p));
+      B[2 * s2] = p[0];
+      B[2 * s2 + 1] = p[1];
+    }
+    if constexpr (S % 2 == 1) {
+      const v2i v = __builtin_amdgcn_raw_buffer_load_b64(rs, boff_last, soff, 0);
+      B[S - 1] = __builtin_bit_cast(double, v);
+    }
+  };
+  static_assert(kLoads >= 1, "loads per interval");
+  double B0[S], B1[S];
+
+  const int nch = (nnei + kC - 1) / kC;
+  int s0 = ((int)(blockIdx.x * 5 + wave * 3) % nch) * kC;
+  uint32_t vm = 0;
+  for (int cc = 0, wbase = -1; cc < nch; ++cc, s0 = s0 + kC < nnei ? s0 + kC : 0) {
+    if (s0 - s0 % (kWindow / NB) != wbase) {  // window of nlist signs holding s0
+      wbase = s0 - s0 % (kWindow / NB);
+      vm = valid_window<NB>(g, i0, wbase, nlist, lane);
+    }
+    int pair;
+    const Tables tb = build_chunk_set<double, double, NB, true, true>(g, ai, i0, s0, wbase, vm,
+                                                                      em, W, lane, &pair);
+    if (tb.n > 0) {
+      // the records of pairs [base, base + np) read their products; each
+      // result replaces its record in LDS
+      auto eval = [&](int base, int np) __attribute__((always_inline)) {
+        wave_sync();
+        if (pair >= base && pair < base + np) {
+          const double* sp = store + (pair - base) * 64;
+          const Rec<double>& rc = zrec<double>(smem, zoff, tb.rank);
+          const double t = rc.t;
+          const double r0 = rc.r[0], r1 = rc.r[1], r2 = rc.r[2], r3 = rc.r[3];
+          double val[4], der[4];
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const Pair<double>* lo = reinterpret_cast<const Pair<double>*>(sp + 16 * k);
+            const Pair<double>* hi = reinterpret_cast<const Pair<double>*>(sp + 16 * k + 8);
+            const Pair<double> c01 = lo[0] + hi[0], c23 = lo[1] + hi[1], c45 = lo[2] + hi[2];
+            double v = c45.y, d = c45.y;
+            v = fma(v, t, c45.x);
+            d = fma(d, t, v);
+            v = fma(v, t, c23.y);
+            d = fma(d, t, v);
+            v = fma(v, t, c23.x);
+            d = fma(d, t, v);
+            v = fma(v, t, c01.y);
+            d = fma(d, t, v);
+            val[k] = fma(v, t, c01.x);
+            der[k] = d;
+          }
+          // clamped records carry a zero row, which removes the derivative term
+          double o0 = fma(r0, der[0], val[0]);
+          o0 = fma(r1, der[1], o0);
+          o0 = fma(r2, der[2], o0);
+          o0 = fma(r3, der[3], o0);
+          Pair<double>* o = reinterpret_cast<Pair<double>*>(
+              __builtin_assume_aligned(smem + zoff + tb.rank * (int)sizeof(Rec<double>), 16));
+          o[0] = Pair<double>{o0, val[1]};
+          o[1] = Pair<double>{val[2], val[3]};
+        }
+        wave_sync();
+      };
+
+      auto next_off = [&](int r) __attribute__((always_inline)) {
+        return key_offset(readlane(tb.vk, min(r, kLanes - 1)));
+      };
+      load_b(next_off(0), B0);
+      int r = 0, base = 0, np = 0;
+      // run r with `cur` loaded; the next run's coefficients go to `nxt`
+      auto run = [&](double (&cur)[S], double (&nxt)[S]) __attribute__((always_inline)) {
+        load_b(next_off(r + 1), nxt);
+        const int Sr = readlane(tb.vs, r);
+        const int Er = r + 1 < kLanes ? readlane(tb.vs, r + 1) : tb.n;
+        int p[2] = {0, 0};
+        p[0] = readlane(tb.vp[0], r);
+        if constexpr (NB > 5) p[1] = readlane(tb.vp[1], r);
+        // one product per atom with records in the run, in atom order
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          const int lo = b == 0 ? Sr : split_at<NB>(p, b);
+          const int hi = b == NB - 1 ? Er : split_at<NB>(p, b + 1);
+          if (lo < hi) {
+            double d = 0.0;
+#pragma unroll
+            for (int s = 0; s < S; ++s) d = mfma4(A[b][s], cur[s], d);
+            store[np * 64 + lane] = d;
+            ++np;
+          }
+        }
+        if (np > kPairSlots - NB) {  // the next run may add NB products
+          eval(base, np);
+          base += np;
+          np = 0;
+        }
+      };
+      for (;;) {
+        run(B0, B1);
+        if (++r == tb.nruns) break;
+        run(B1, B0);
+        if (++r == tb.nruns) break;
+      }
+      if (np > 0) eval(base, np);
+    }
+    // each lane writes the dE/dR~ row of its own slot (zero for padding)
+    if (tb.rank >= -1) {
+      double v[4] = {0.0, 0.0, 0.0, 0.0};
+      if (tb.rank >= 0) {
+        const double* src = reinterpret_cast<const double*>(&zrec<double>(smem, zoff, tb.rank));
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = src[k];
+      }
+      store_row(dR + ((size_t)(i0 + lane / kC) * nnei + s0 + lane % kC) * 4, v);
+    }
+    wave_sync();
+  }
+}
+
 bool dtype_ok(int dt) { return dt == DPC_F64 || dt == DPC_F32 || dt == DPC_F32_ACC64; }
 
 thread_local hipError_t g_last_hip = hipSuccess;
@@ -870,9 +1098,45 @@ int launch_fwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
   return launch_status();
 }
 
+// float64 with M1 <= 112: the matrix-core kernel, ceil(M1 / 8) K steps per channel half
+int launch_bwd_mfma(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
+                    const int* nlist, const void* em, const void* dT, void* dR) {
+  const int S = (g.m1 + 7) / 8;
+  constexpr int NB = kMfmaAtoms;
+  const dim3 grid((g.nloc + kWaves * NB - 1) / (kWaves * NB)), block(64 * kWaves);
+  const size_t shm = kWaves * bwdm_wave_bytes();
+  (void)hipGetLastError();  // report only what this launch raises
+  auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, grid, block, shm, s, g, (const double*)coeff, atype, nlist,
+                       (const double*)em, (const double*)dT, (double*)dR);
+  };
+  switch (S) {
+    case 1: go(se_a_bwd_mfma_kernel<1>); break;
+    case 2: go(se_a_bwd_mfma_kernel<2>); break;
+    case 3: go(se_a_bwd_mfma_kernel<3>); break;
+    case 4: go(se_a_bwd_mfma_kernel<4>); break;
+    case 5: go(se_a_bwd_mfma_kernel<5>); break;
+    case 6: go(se_a_bwd_mfma_kernel<6>); break;
+    case 7: go(se_a_bwd_mfma_kernel<7>); break;
+    case 8: go(se_a_bwd_mfma_kernel<8>); break;
+    case 9: go(se_a_bwd_mfma_kernel<9>); break;
+    case 10: go(se_a_bwd_mfma_kernel<10>); break;
+    case 11: go(se_a_bwd_mfma_kernel<11>); break;
+    case 12: go(se_a_bwd_mfma_kernel<12>); break;
+    case 13: go(se_a_bwd_mfma_kernel<13>); break;
+    default: go(se_a_bwd_mfma_kernel<14>); break;
+  }
+  return launch_status();
+}
+
 template <typename TI, typename TA>
 int launch_bwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype, const int* nlist,
                const void* em, const void* dT, void* dR) {
+#ifndef DPC_BWD_VALU_ONLY
+  if constexpr (sizeof(TI) == 8 && sizeof(TA) == 8) {
+    if (g.m1 <= 112) return launch_bwd_mfma(s, g, coeff, atype, nlist, em, dT, dR);
+  }
+#endif
   constexpr int NB = DPC_BWD_ATOMS_PER_WAVE;
   static_assert(NB == 1 || NB == 2 || NB == 4 || NB == 8, "atoms per wave: 1, 2, 4 or 8");
   const dim3 grid((g.nloc + kWaves * NB - 1) / (kWaves * NB)), block(64 * kWaves);
