@@ -171,9 +171,9 @@ def main():
     step_s = wall / args.steps
     peak = PEAK_TFLOPS[dtype]
     tflops = (flop_fwd + flop_bwd) / step_s / 1e12
-    # float64 backward passes with M1 <= 112 run on the matrix-core kernel (the
+    # float64 backward passes with M1 <= 128 run on the matrix-core kernel (the
     # library's rule); both FP64 peaks of MI355X, vector and matrix, are 78.6 TFLOP/s
-    bwd_mfma = dtype == "f64" and cfg.widths[-1] <= 112
+    bwd_mfma = dtype == "f64" and cfg.widths[-1] <= 128
     bwd_name = "se_a_bwd_mfma_kernel" if bwd_mfma else "se_a_bwd_kernel"
     dom = bwd_name if bwd_ms >= fwd_ms else "se_a_fwd_kernel"
     bound = "mfma" if dom == "se_a_bwd_mfma_kernel" else "alu"

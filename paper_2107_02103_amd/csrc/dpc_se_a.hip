@@ -802,49 +802,57 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// backward, float64, M1 <= 112: channel sums on the matrix cores
+// backward, float64, M1 <= 128: channel sums on the matrix cores
 // ---------------------------------------------------------------------------
 // For one interval (coefficients C[m][q], g_m(t) = sum_q C[m][q] t^q) and
 // one atom (dE/dT rows dT[m][k]) both channel sums of a record factor
 // through the 4 x 6 matrix P[k][q] = sum_m dT[m][k] C[m][q]:
 //   sum_m dT[m][k] g_m(t)                  = sum_q t^q P[k][q]
 //   sum_m g'_m(t) sum_k' dT[m][k'] R~[k']  = sum_k' R~[k'] sum_q q t^(q-1) P[k'][q].
-// P of each (interval, atom) pair of a chunk set is one chain of
-// v_mfma_f64_4x4x4f64, and each record then costs a few dozen operations in
-// the lane that owns its slot.
+// P of each (interval, atom) pair of a chunk set comes from two chains of
+// v_mfma_f64_4x4x4f64 (powers 0-3 and 4-7, of which 6 and 7 are not used),
+// and each record then costs a few dozen operations in the lane that owns
+// its slot.
 //
 // v_mfma_f64_4x4x4f64 computes four independent 4x4 products D_b = A_b B_b
 // (+ C_b).  Lane L = 16 kk + 4 b + x holds A_b[x][kk] and B_b[kk][x]; D_b[i][j]
-// sits in lane 16 i + 4 b + j (measured on gfx950).  Here block b = 2 h + g:
-// g selects the powers 4g .. 4g+3 (6 and 7 are not used), h the half of the
-// channels, 4S channels each.  K step s < 2 (S / 2) of half h covers the
-// channels h*4S + 8(s/2) + 2kk + s%2, so that one 16-byte load of a lane
-// brings its coefficients for two consecutive K steps; for odd S the last
-// step covers h*4S + 4(S-1) + kk.  The two halves' products are summed when a
-// record reads P.
+// sits in lane 16 i + 4 b + j (measured on gfx950).  Block b is a quarter of
+// the channels, 4S channels each; A_b = dT^T of the quarter (rows k), B_b the
+// quarter's coefficients (columns q).  K step s < 2 (S / 2) of quarter h
+// covers the channels h*4S + 8(s/2) + 2kk + s%2, so that one 16-byte load of
+// a lane brings its coefficients for two consecutive K steps; for odd S the
+// last step covers h*4S + 4(S-1) + kk.  The four quarters' products are summed
+// across lanes (DPP row shifts) into the lanes of quarter 3, which store P.
 constexpr int kPairSlots = 16;     // (interval, atom) products held in LDS at once
+constexpr int kMfmaAtoms = 4;      // atoms per wavefront in the matrix-core kernel
 
 __host__ __device__ constexpr size_t bwdm_wave_bytes() {
-  return align16(sizeof(WaveLds<double>)) + (size_t)kPairSlots * 64 * sizeof(double);
+  return align16(sizeof(WaveLds<double>)) + (size_t)kPairSlots * 32 * sizeof(double);
 }
 
 __device__ __forceinline__ double mfma4(double a, double b, double c) {
   return __builtin_amdgcn_mfma_f64_4x4x4f64(a, b, c, 0, 0, 0);
 }
 
-constexpr int kMfmaAtoms = 4;      // atoms per wavefront in the matrix-core kernel
+// v from lane l - N of the same row of 16 lanes (0 for the first N lanes)
+template <int N>
+__device__ __forceinline__ double row_shr(double v) {
+  const v2i a = __builtin_bit_cast(v2i, v);
+  v2i r;
+  r.x = __builtin_amdgcn_update_dpp(0, a.x, 0x110 | N, 0xF, 0xF, true);
+  r.y = __builtin_amdgcn_update_dpp(0, a.y, 0x110 | N, 0xF, 0xF, true);
+  return __builtin_bit_cast(double, r);
+}
 
-// 4 atoms' dE/dT operands and two coefficient sets take more than 168
-// registers: two wavefronts per SIMD
+// up to 128 channels: registers capped so that 3 wavefronts fit on a SIMD
 template <int S>
-__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(3)))
 void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
                           const int* __restrict__ atype, const int* __restrict__ nlist,
                           const double* __restrict__ em, const double* __restrict__ dT,
                           double* __restrict__ dR) {
-  static_assert(S >= 1 && S <= 14, "K steps per channel half");
-  constexpr int S2 = S / 2;           // 16-byte loads per interval
-  constexpr int kLoads = S2 + S % 2;  // loads per interval
+  static_assert(S >= 1 && S <= 8, "K steps per channel quarter");
+  constexpr int S2 = S / 2;           // 16-byte loads per chain and interval
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int NB = kMfmaAtoms;
   constexpr int kC = kLanes / NB;
@@ -859,14 +867,19 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
   double* const store = reinterpret_cast<double*>(wb + align16(sizeof(WaveLds<double>)));
   const __amdgpu_buffer_rsrc_t rs = make_rsrc(coeff, g.coeff_bytes);
 
-  // this lane's place in the MFMA operands
-  const int kk = lane >> 4, h = (lane >> 3) & 1, x = lane & 3;
-  const int q = min(4 * ((lane >> 2) & 1) + x, 5);   // power held in B (6, 7 repeat 5)
+  // this lane's place in the MFMA operands: K index kk, block = channel quarter h
+  const int kk = lane >> 4, h = (lane >> 2) & 3, x = lane & 3;
   const int ch0 = h * 4 * S + 2 * kk;                 // channel of K step 0
-  const int boff = (q * ld + ch0) * (int)sizeof(double);
-  const int boff_last = (q * ld + h * 4 * S + 4 * (S - 1) + kk) * (int)sizeof(double);
+  const int chl = h * 4 * S + 4 * (S - 1) + kk;       // channel of the last step, S odd
+  int boff[2], boffl[2];
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const int q = min(4 * c + x, 5);                  // power held in B (6, 7 repeat 5)
+    boff[c] = (q * ld + ch0) * (int)sizeof(double);
+    boffl[c] = (q * ld + chl) * (int)sizeof(double);
+  }
   auto channel = [&](int s) __attribute__((always_inline)) {
-    return s < 2 * S2 ? ch0 + 8 * (s >> 1) + (s & 1) : h * 4 * S + 4 * (S - 1) + kk;
+    return s < 2 * S2 ? ch0 + 8 * (s >> 1) + (s & 1) : chl;
   };
 
   // A operands: dT of the wave's atoms, transposed, zero past M1
@@ -893,24 +906,26 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
     }
   }
 
-  // B operands of one interval: coefficients at element offset `off`
-  auto load_b = [&](int off, double (&B)[S]) __attribute__((always_inline)) {
+  // B operands of one interval (powers 0-3 and 4-5): coefficients at element offset `off`
+  auto load_b = [&](int off, double (&B)[2][S]) __attribute__((always_inline)) {
     const int soff = off * (int)sizeof(double);
 #pragma unroll
-    for (int s2 = 0; s2 < S2; ++s2) {
-      const v4i v = __builtin_amdgcn_raw_buffer_load_b128(rs, boff, soff + 64 * s2, 0);
-      double p[2];
-      __builtin_memcpy(p, &v, sizeof(p));
-      B[2 * s2] = p[0];
-      B[2 * s2 + 1] = p[1];
-    }
-    if constexpr (S % 2 == 1) {
-      const v2i v = __builtin_amdgcn_raw_buffer_load_b64(rs, boff_last, soff, 0);
-      B[S - 1] = __builtin_bit_cast(double, v);
+    for (int c = 0; c < 2; ++c) {
+#pragma unroll
+      for (int s2 = 0; s2 < S2; ++s2) {
+        const v4i v = __builtin_amdgcn_raw_buffer_load_b128(rs, boff[c], soff + 64 * s2, 0);
+        double p[2];
+        __builtin_memcpy(p, &v, sizeof(p));
+        B[c][2 * s2] = p[0];
+        B[c][2 * s2 + 1] = p[1];
+      }
+      if constexpr (S % 2 == 1) {
+        const v2i v = __builtin_amdgcn_raw_buffer_load_b64(rs, boffl[c], soff, 0);
+        B[c][S - 1] = __builtin_bit_cast(double, v);
+      }
     }
   };
-  static_assert(kLoads >= 1, "loads per interval");
-  double B0[S], B1[S];
+  double BA[2][S], BB[2][S];
 
   const int nch = (nnei + kC - 1) / kC;
   int s0 = ((int)(blockIdx.x * 5 + wave * 3) % nch) * kC;
@@ -929,16 +944,15 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
       auto eval = [&](int base, int np) __attribute__((always_inline)) {
         wave_sync();
         if (pair >= base && pair < base + np) {
-          const double* sp = store + (pair - base) * 64;
+          const double* sp = store + (pair - base) * 32;
           const Rec<double>& rc = zrec<double>(smem, zoff, tb.rank);
           const double t = rc.t;
           const double r0 = rc.r[0], r1 = rc.r[1], r2 = rc.r[2], r3 = rc.r[3];
           double val[4], der[4];
 #pragma unroll
           for (int k = 0; k < 4; ++k) {
-            const Pair<double>* lo = reinterpret_cast<const Pair<double>*>(sp + 16 * k);
-            const Pair<double>* hi = reinterpret_cast<const Pair<double>*>(sp + 16 * k + 8);
-            const Pair<double> c01 = lo[0] + hi[0], c23 = lo[1] + hi[1], c45 = lo[2] + hi[2];
+            const Pair<double>* pk = reinterpret_cast<const Pair<double>*>(sp + 8 * k);
+            const Pair<double> c01 = pk[0], c23 = pk[1], c45 = pk[2];
             double v = c45.y, d = c45.y;
             v = fma(v, t, c45.x);
             d = fma(d, t, v);
@@ -967,26 +981,37 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
       auto next_off = [&](int r) __attribute__((always_inline)) {
         return key_offset(readlane(tb.vk, min(r, kLanes - 1)));
       };
-      load_b(next_off(0), B0);
+      load_b(next_off(0), BA);
       int r = 0, base = 0, np = 0;
       // run r with `cur` loaded; the next run's coefficients go to `nxt`
-      auto run = [&](double (&cur)[S], double (&nxt)[S]) __attribute__((always_inline)) {
+      auto run = [&](double (&cur)[2][S], double (&nxt)[2][S]) __attribute__((always_inline)) {
         load_b(next_off(r + 1), nxt);
         const int Sr = readlane(tb.vs, r);
         const int Er = r + 1 < kLanes ? readlane(tb.vs, r + 1) : tb.n;
         int p[2] = {0, 0};
         p[0] = readlane(tb.vp[0], r);
-        if constexpr (NB > 5) p[1] = readlane(tb.vp[1], r);
         // one product per atom with records in the run, in atom order
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
           const int lo = b == 0 ? Sr : split_at<NB>(p, b);
           const int hi = b == NB - 1 ? Er : split_at<NB>(p, b + 1);
           if (lo < hi) {
-            double d = 0.0;
+            double d0 = 0.0, d1 = 0.0;
 #pragma unroll
-            for (int s = 0; s < S; ++s) d = mfma4(A[b][s], cur[s], d);
-            store[np * 64 + lane] = d;
+            for (int s = 0; s < S; ++s) {
+              d0 = mfma4(A[b][s], cur[0][s], d0);
+              d1 = mfma4(A[b][s], cur[1][s], d1);
+            }
+            // sum the four channel quarters into the lanes of quarter 3
+            d0 += row_shr<4>(d0);
+            d1 += row_shr<4>(d1);
+            d0 += row_shr<8>(d0);
+            d1 += row_shr<8>(d1);
+            if (h == 3) {
+              double* o = store + np * 32 + 8 * kk + x;   // P[k = kk][q]
+              o[0] = d0;
+              o[4] = d1;
+            }
             ++np;
           }
         }
@@ -997,9 +1022,9 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
         }
       };
       for (;;) {
-        run(B0, B1);
+        run(BA, BB);
         if (++r == tb.nruns) break;
-        run(B1, B0);
+        run(BB, BA);
         if (++r == tb.nruns) break;
       }
       if (np > 0) eval(base, np);
@@ -1098,10 +1123,10 @@ int launch_fwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
   return launch_status();
 }
 
-// float64 with M1 <= 112: the matrix-core kernel, ceil(M1 / 8) K steps per channel half
+// float64 with M1 <= 128: the matrix-core kernel, ceil(M1 / 16) K steps per channel quarter
 int launch_bwd_mfma(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
                     const int* nlist, const void* em, const void* dT, void* dR) {
-  const int S = (g.m1 + 7) / 8;
+  const int S = (g.m1 + 15) / 16;
   constexpr int NB = kMfmaAtoms;
   const dim3 grid((g.nloc + kWaves * NB - 1) / (kWaves * NB)), block(64 * kWaves);
   const size_t shm = kWaves * bwdm_wave_bytes();
@@ -1118,13 +1143,7 @@ int launch_bwd_mfma(hipStream_t s, const Geo& g, const void* coeff, const int* a
     case 5: go(se_a_bwd_mfma_kernel<5>); break;
     case 6: go(se_a_bwd_mfma_kernel<6>); break;
     case 7: go(se_a_bwd_mfma_kernel<7>); break;
-    case 8: go(se_a_bwd_mfma_kernel<8>); break;
-    case 9: go(se_a_bwd_mfma_kernel<9>); break;
-    case 10: go(se_a_bwd_mfma_kernel<10>); break;
-    case 11: go(se_a_bwd_mfma_kernel<11>); break;
-    case 12: go(se_a_bwd_mfma_kernel<12>); break;
-    case 13: go(se_a_bwd_mfma_kernel<13>); break;
-    default: go(se_a_bwd_mfma_kernel<14>); break;
+    default: go(se_a_bwd_mfma_kernel<8>); break;
   }
   return launch_status();
 }
@@ -1134,7 +1153,7 @@ int launch_bwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
                const void* em, const void* dT, void* dR) {
 #ifndef DPC_BWD_VALU_ONLY
   if constexpr (sizeof(TI) == 8 && sizeof(TA) == 8) {
-    if (g.m1 <= 112) return launch_bwd_mfma(s, g, coeff, atype, nlist, em, dT, dR);
+    if (g.m1 <= 128) return launch_bwd_mfma(s, g, coeff, atype, nlist, em, dT, dR);
   }
 #endif
   constexpr int NB = DPC_BWD_ATOMS_PER_WAVE;

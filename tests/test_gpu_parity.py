@@ -158,7 +158,12 @@ def _synthetic(nloc, sel, m1, m2, seed, lo=-0.6, L1=300, L2=30, d1=0.01, d2=0.1)
                                        ((130,), 1, 1), ((1,), 100, 100),
                                        # more slots than one window of nlist signs (512 or
                                        # 1024 per atom), ragged at the end
-                                       ((700, 900), 100, 16), ((2100,), 64, 16)])
+                                       ((700, 900), 100, 16), ((2100,), 64, 16),
+                                       # K steps of the float64 matrix-core backward: odd
+                                       # and even per channel quarter, its largest M1 and
+                                       # the first M1 past it
+                                       ((77,), 17, 4), ((40, 33), 128, 16), ((20,), 113, 16),
+                                       ((50,), 129, 8)])
 def test_edge_shapes_and_ranges(sel, m1, m2):
     # ragged nnei, m1 not a multiple of 64 (and m1 > 128), m2 = m1, a single
     # channel, inputs below lo and beyond the band (clamped), empty atoms
