@@ -136,7 +136,10 @@ int dpc_se_a_tab_fwd(void* stream, dpc_dtype dtype, int nloc, int ntypes, const 
 /* Backward of T (forces need dE/dR~, paper Sec. II):
  *   dE/dR~_ij[k] = sum_m dE/dT_i[m][k] g_m(x) + (k == 0) sum_m g'_m(x) w_m,
  *   w_m = sum_k' dE/dT_i[m][k'] R~_ij[k'],  x = R~_ij[0],
- * for valid j; padded rows are written as 0.
+ * for valid j; padded rows are written as 0.  For DPC_F64 with m1 <= 128 the
+ * channel sums are formed per (interval, atom) pair on the matrix cores, as
+ * P[k][q] = sum_m dE/dT_i[m][k] C[m][q] followed by a polynomial in t per
+ * neighbour: the same sums in another order of rounding.
  *   dE_dT    device [nloc][m1][4] (float64 for DPC_F64, else float32)
  *   dE_dem   device out [nloc][nnei][4] (float32 only for DPC_F32), 16-byte aligned
  * Other arguments as dpc_se_a_tab_fwd.                                      */

@@ -823,11 +823,23 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
 // a lane brings its coefficients for two consecutive K steps; for odd S the
 // last step covers h*4S + 4(S-1) + kk.  The four quarters' products are summed
 // across lanes (DPP row shifts) into the lanes of quarter 3, which store P.
-constexpr int kPairSlots = 16;     // (interval, atom) products held in LDS at once
+//
+// The B operands are not loaded from the table directly (two power groups,
+// 8 loads per interval for M1 = 100, a quarter of them repeating power 5):
+// an interval's 6 rows are fetched densely by NS wave-wide 16-byte loads (5
+// for M1 = 100), written to a per-wavefront LDS slot, and read from there.
+// The vector memory address unit, which bounds this kernel, then does 5/8
+// of the work.
 constexpr int kMfmaAtoms = 4;      // atoms per wavefront in the matrix-core kernel
 
-__host__ __device__ constexpr size_t bwdm_wave_bytes() {
-  return align16(sizeof(WaveLds<double>)) + (size_t)kPairSlots * 32 * sizeof(double);
+// An interval's coefficients (6 rows of ld) are staged in LDS by NS wave-wide
+// 16-byte loads; (interval, atom) products held in LDS at once: pair_slots.
+// Four wavefronts' LDS stays at or below 53,312 bytes, so that three
+// workgroups share a CU (measured: 53,824 bytes leave room for two).
+__host__ __device__ constexpr int pair_slots(int ns) { return ns <= 5 ? 16 : (ns == 6 ? 12 : 8); }
+__host__ __device__ constexpr size_t bwdm_wave_bytes(int ns) {
+  return align16(sizeof(WaveLds<double>)) + (size_t)pair_slots(ns) * 32 * sizeof(double) +
+         (size_t)ns * 1024;
 }
 
 __device__ __forceinline__ double mfma4(double a, double b, double c) {
@@ -845,7 +857,7 @@ __device__ __forceinline__ double row_shr(double v) {
 }
 
 // up to 128 channels: registers capped so that 3 wavefronts fit on a SIMD
-template <int S>
+template <int S, int NS>
 __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(3)))
 void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
                           const int* __restrict__ atype, const int* __restrict__ nlist,
@@ -861,10 +873,13 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
   const int i0 = __builtin_amdgcn_readfirstlane((blockIdx.x * kWaves + wave) * NB);
   if (i0 >= g.nloc) return;
   const int nnei = g.nnei, m1 = g.m1, ld = g.ld;
-  const uint32_t zoff = __builtin_amdgcn_readfirstlane(wave * (uint32_t)bwdm_wave_bytes());
+  constexpr int kPairSlots = pair_slots(NS);
+  const uint32_t zoff = __builtin_amdgcn_readfirstlane(wave * (uint32_t)bwdm_wave_bytes(NS));
   unsigned char* wb = smem + zoff;
   WaveLds<double>& W = *reinterpret_cast<WaveLds<double>*>(wb);
   double* const store = reinterpret_cast<double*>(wb + align16(sizeof(WaveLds<double>)));
+  const uint32_t slot = zoff + (uint32_t)(align16(sizeof(WaveLds<double>)) +
+                                          (size_t)kPairSlots * 32 * sizeof(double));
   const __amdgpu_buffer_rsrc_t rs = make_rsrc(coeff, g.coeff_bytes);
 
   // this lane's place in the MFMA operands: K index kk, block = channel quarter h
@@ -875,7 +890,7 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
     const int q = min(4 * c + x, 5);                  // power held in B (6, 7 repeat 5)
-    boff[c] = (q * ld + ch0) * (int)sizeof(double);
+    boff[c] = (q * ld + ch0) * (int)sizeof(double);    // inside the LDS slot
     boffl[c] = (q * ld + chl) * (int)sizeof(double);
   }
   auto channel = [&](int s) __attribute__((always_inline)) {
@@ -906,26 +921,39 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
     }
   }
 
-  // B operands of one interval (powers 0-3 and 4-5): coefficients at element offset `off`
-  auto load_b = [&](int off, double (&B)[2][S]) __attribute__((always_inline)) {
+  // An interval's coefficients pass through registers (`stg`, 16 bytes per
+  // lane and load, in order) into the wave's LDS slot; the B operands are
+  // read from there.  Past the 6 rows the slot holds whatever follows in the
+  // table (or zeros past its end): finite values met only by zero A operands.
+  auto fetch = [&](int off, v4i (&stg)[NS]) __attribute__((always_inline)) {
     const int soff = off * (int)sizeof(double);
+#pragma unroll
+    for (int i = 0; i < NS; ++i)
+      stg[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, lane * 16, soff + 1024 * i, 0);
+  };
+  auto put = [&](const v4i (&stg)[NS]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < NS; ++i)
+      *reinterpret_cast<v4i*>(__builtin_assume_aligned(smem + slot + 1024 * i + lane * 16, 16)) =
+          stg[i];
+  };
+  auto read_b = [&](double (&B)[2][S]) __attribute__((always_inline)) {
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
 #pragma unroll
       for (int s2 = 0; s2 < S2; ++s2) {
-        const v4i v = __builtin_amdgcn_raw_buffer_load_b128(rs, boff[c], soff + 64 * s2, 0);
-        double p[2];
-        __builtin_memcpy(p, &v, sizeof(p));
-        B[c][2 * s2] = p[0];
-        B[c][2 * s2 + 1] = p[1];
+        const Pair<double> v = *reinterpret_cast<const Pair<double>*>(
+            __builtin_assume_aligned(smem + slot + boff[c] + 64 * s2, 16));
+        B[c][2 * s2] = v.x;
+        B[c][2 * s2 + 1] = v.y;
       }
-      if constexpr (S % 2 == 1) {
-        const v2i v = __builtin_amdgcn_raw_buffer_load_b64(rs, boffl[c], soff, 0);
-        B[c][S - 1] = __builtin_bit_cast(double, v);
-      }
+      if constexpr (S % 2 == 1)
+        B[c][S - 1] = *reinterpret_cast<const double*>(
+            __builtin_assume_aligned(smem + slot + boffl[c], 8));
     }
   };
-  double BA[2][S], BB[2][S];
+  v4i stg[NS];
+  double Bc[2][S];
 
   const int nch = (nnei + kC - 1) / kC;
   int s0 = ((int)(blockIdx.x * 5 + wave * 3) % nch) * kC;
@@ -981,11 +1009,14 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
       auto next_off = [&](int r) __attribute__((always_inline)) {
         return key_offset(readlane(tb.vk, min(r, kLanes - 1)));
       };
-      load_b(next_off(0), BA);
+      fetch(next_off(0), stg);
       int r = 0, base = 0, np = 0;
-      // run r with `cur` loaded; the next run's coefficients go to `nxt`
-      auto run = [&](double (&cur)[2][S], double (&nxt)[2][S]) __attribute__((always_inline)) {
-        load_b(next_off(r + 1), nxt);
+      for (;;) {
+        // run r: its coefficients go from `stg` to LDS, the next run's into `stg`
+        put(stg);
+        fetch(next_off(r + 1), stg);
+        wave_sync();
+        read_b(Bc);
         const int Sr = readlane(tb.vs, r);
         const int Er = r + 1 < kLanes ? readlane(tb.vs, r + 1) : tb.n;
         int p[2] = {0, 0};
@@ -999,8 +1030,8 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
             double d0 = 0.0, d1 = 0.0;
 #pragma unroll
             for (int s = 0; s < S; ++s) {
-              d0 = mfma4(A[b][s], cur[0][s], d0);
-              d1 = mfma4(A[b][s], cur[1][s], d1);
+              d0 = mfma4(A[b][s], Bc[0][s], d0);
+              d1 = mfma4(A[b][s], Bc[1][s], d1);
             }
             // sum the four channel quarters into the lanes of quarter 3
             d0 += row_shr<4>(d0);
@@ -1015,16 +1046,12 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
             ++np;
           }
         }
+        wave_sync();   // the slot is rewritten by the next run
         if (np > kPairSlots - NB) {  // the next run may add NB products
           eval(base, np);
           base += np;
           np = 0;
         }
-      };
-      for (;;) {
-        run(BA, BB);
-        if (++r == tb.nruns) break;
-        run(BB, BA);
         if (++r == tb.nruns) break;
       }
       if (np > 0) eval(base, np);
@@ -1123,27 +1150,36 @@ int launch_fwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
   return launch_status();
 }
 
-// float64 with M1 <= 128: the matrix-core kernel, ceil(M1 / 16) K steps per channel quarter
+// float64 with M1 <= 128: the matrix-core kernel, ceil(M1 / 16) K steps per
+// channel quarter, an interval staged by ceil((48 ld + 128) / 1024) loads
+template <int S>
+void launch_mfma_s(hipStream_t s, const Geo& g, dim3 grid, dim3 block, const void* coeff,
+                   const int* atype, const int* nlist, const void* em, const void* dT, void* dR) {
+  const int ns = (48 * g.ld + 128 + 1023) / 1024;
+  auto go = [&](auto kern, size_t wave_bytes) {
+    hipLaunchKernelGGL(kern, grid, block, kWaves * wave_bytes, s, g, (const double*)coeff,
+                       atype, nlist, (const double*)em, (const double*)dT, (double*)dR);
+  };
+  constexpr int lo = (48 * (16 * S - 12) + 128 + 1023) / 1024;   // smallest ld of this S
+  if (ns <= lo) go(se_a_bwd_mfma_kernel<S, lo>, bwdm_wave_bytes(lo));
+  else go(se_a_bwd_mfma_kernel<S, lo + 1>, bwdm_wave_bytes(lo + 1));
+}
+
 int launch_bwd_mfma(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
                     const int* nlist, const void* em, const void* dT, void* dR) {
   const int S = (g.m1 + 15) / 16;
   constexpr int NB = kMfmaAtoms;
   const dim3 grid((g.nloc + kWaves * NB - 1) / (kWaves * NB)), block(64 * kWaves);
-  const size_t shm = kWaves * bwdm_wave_bytes();
   (void)hipGetLastError();  // report only what this launch raises
-  auto go = [&](auto kern) {
-    hipLaunchKernelGGL(kern, grid, block, shm, s, g, (const double*)coeff, atype, nlist,
-                       (const double*)em, (const double*)dT, (double*)dR);
-  };
   switch (S) {
-    case 1: go(se_a_bwd_mfma_kernel<1>); break;
-    case 2: go(se_a_bwd_mfma_kernel<2>); break;
-    case 3: go(se_a_bwd_mfma_kernel<3>); break;
-    case 4: go(se_a_bwd_mfma_kernel<4>); break;
-    case 5: go(se_a_bwd_mfma_kernel<5>); break;
-    case 6: go(se_a_bwd_mfma_kernel<6>); break;
-    case 7: go(se_a_bwd_mfma_kernel<7>); break;
-    default: go(se_a_bwd_mfma_kernel<8>); break;
+    case 1: launch_mfma_s<1>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
+    case 2: launch_mfma_s<2>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
+    case 3: launch_mfma_s<3>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
+    case 4: launch_mfma_s<4>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
+    case 5: launch_mfma_s<5>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
+    case 6: launch_mfma_s<6>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
+    case 7: launch_mfma_s<7>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
+    default: launch_mfma_s<8>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
   }
   return launch_status();
 }
