@@ -93,17 +93,20 @@ int dpc_version(void);
  * In:  ranges[p].{lo,d1,d2,L1,L2}.  Out: ranges[p].offset (elements) and
  * *total_bytes, the size of the coefficient buffer for `dtype` (DPC_F32 and
  * DPC_F32_ACC64 store float32 coefficients).  The layout of one pair is
- * [L1 + L2][6][DPC_TABLE_LD(m1)]: for interval l, row q holds the
- * coefficient of t^q of every channel, t = x - (left node of l); rows are
- * padded with zeros to a multiple of 4 channels so that the kernels can use
- * 16-byte loads without leaving the buffer.                                 */
+ * [L1 + L2][3][DPC_TABLE_LD(m1)][2]: interval l holds 6 * ld elements, and
+ * the coefficient of t^q of channel m, t = x - (left node of l), is element
+ * DPC_TABLE_AT(ld, q, m) of it, so the coefficients of t^(2j) and t^(2j+1)
+ * of one channel are adjacent (one 16-byte float64 load brings both).
+ * Channels are padded with zeros to a multiple of 4 so that the kernels can
+ * use 16-byte loads without leaving the buffer.                             */
 #define DPC_TABLE_LD(m1) (((m1) + 3) / 4 * 4)
+#define DPC_TABLE_AT(ld, q, m) (((q) >> 1) * 2 * (ld) + 2 * (m) + ((q) & 1))
 int dpc_table_layout(int npair, int m1, dpc_range* ranges, dpc_dtype dtype,
                      size_t* total_bytes);
 
 /* Paper Sec. II, Eqs. for the constraints y, y', y'' at both nodes of each
  * interval and the closed forms for a..f: tabulate `net` (m1 = last width)
- * over `range` and write its [L1 + L2][6][DPC_TABLE_LD(m1)] coefficients to `host_out`
+ * over `range` and write its (L1 + L2) * 6 * DPC_TABLE_LD(m1) coefficients to `host_out`
  * (host memory, float64 or float32 per `dtype`).  The first and second
  * derivatives of the net are computed in forward mode in float64.          */
 int dpc_build_table(const dpc_net* net, const dpc_range* range, dpc_dtype dtype,

@@ -95,6 +95,13 @@ def table_ld(m1):
     return (int(m1) + 3) // 4 * 4
 
 
+def unpack_table(buf, n_intervals, ld):
+    """View of one pair's coefficients as [interval][power q][channel]
+    (the buffer holds [interval][q // 2][channel][q % 2], DPC_TABLE_AT in dpc.h)."""
+    a = np.asarray(buf).reshape(n_intervals, 3, ld, 2)
+    return a.transpose(0, 1, 3, 2).reshape(n_intervals, 6, ld)
+
+
 def make_ranges(lo, d1, L1, d2, L2):
     """ctypes array of dpc_range from per-pair sequences."""
     n = len(lo)

@@ -157,43 +157,36 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const TI* p, int byt
 }
 
 // Coefficients of t^q (q = 0..5) of the lane's CPL channels of the interval
-// whose rows start at element `off`; voff = byte offset of the lane's first
-// channel inside a row.  Every lane loads (lanes without channels read the
-// last row entries again), so the number of loads in flight is fixed.
+// whose coefficients start at element `off`; voff = byte offset of the lane's
+// first channel inside a power pair (see DPC_TABLE_AT: power pair j holds
+// (t^2j, t^(2j+1)) per channel, so the lane reads 2 * CPL consecutive
+// elements per pair).  Every lane loads (lanes without channels read the
+// last entries again), so the number of loads in flight is fixed.
 template <typename TI, int CPL>
 __device__ __forceinline__ void load_coef(__amdgpu_buffer_rsrc_t rs, int off, int ld, int voff,
                                           TI (&cf)[6][CPL]) {
-  constexpr int kBytes = CPL * (int)sizeof(TI);
+  constexpr int kBytes = 2 * CPL * (int)sizeof(TI);     // per power pair
+  constexpr int kLoads = kBytes >= 16 ? kBytes / 16 : 1;
+  constexpr int kPer = kBytes >= 16 ? 16 / (int)sizeof(TI) : 2 * CPL;   // elements per load
   const int soff = off * (int)sizeof(TI);
 #pragma unroll
-  for (int q = 0; q < 6; ++q) {
-    const int vo = voff + q * ld * (int)sizeof(TI);
-    if constexpr (kBytes == 32) {
-      const v4i a = __builtin_amdgcn_raw_buffer_load_b128(rs, vo, soff, 0);
-      const v4i b = __builtin_amdgcn_raw_buffer_load_b128(rs, vo + 16, soff, 0);
-      TI pa[CPL / 2], pb[CPL / 2];
-      __builtin_memcpy(pa, &a, sizeof(pa));
-      __builtin_memcpy(pb, &b, sizeof(pb));
+  for (int j = 0; j < 3; ++j) {
+    const int vo = voff + j * 2 * ld * (int)sizeof(TI);
+    TI e[2 * CPL];
 #pragma unroll
-      for (int h = 0; h < CPL / 2; ++h) {
-        cf[q][h] = pa[h];
-        cf[q][h + CPL / 2] = pb[h];
+    for (int i = 0; i < kLoads; ++i) {
+      if constexpr (kBytes >= 16) {
+        const v4i a = __builtin_amdgcn_raw_buffer_load_b128(rs, vo + 16 * i, soff, 0);
+        __builtin_memcpy(e + kPer * i, &a, 16);
+      } else {
+        const v2i a = __builtin_amdgcn_raw_buffer_load_b64(rs, vo, soff, 0);
+        __builtin_memcpy(e, &a, 8);
       }
-    } else if constexpr (kBytes == 16) {
-      const v4i a = __builtin_amdgcn_raw_buffer_load_b128(rs, vo, soff, 0);
-      TI pa[CPL];
-      __builtin_memcpy(pa, &a, sizeof(pa));
+    }
 #pragma unroll
-      for (int h = 0; h < CPL; ++h) cf[q][h] = pa[h];
-    } else if constexpr (kBytes == 8) {
-      const v2i a = __builtin_amdgcn_raw_buffer_load_b64(rs, vo, soff, 0);
-      TI pa[CPL];
-      __builtin_memcpy(pa, &a, sizeof(pa));
-#pragma unroll
-      for (int h = 0; h < CPL; ++h) cf[q][h] = pa[h];
-    } else {
-      const int a = __builtin_amdgcn_raw_buffer_load_b32(rs, vo, soff, 0);
-      cf[q][0] = __builtin_bit_cast(TI, a);
+    for (int h = 0; h < CPL; ++h) {
+      cf[2 * j][h] = e[2 * h];
+      cf[2 * j + 1][h] = e[2 * h + 1];
     }
   }
 }
@@ -334,26 +327,32 @@ __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[
     bool bad = false;
     if (sl + 1 < cnt_a) bad = lk[lane] > lk[lane + 1];
     const bool sorted = __ballot(bad) == 0;
-    if (valid) {
+    int cnt[NB];
 #pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const int cnt_b = __popcll((m >> (b * kC)) & seg);
-        if (sorted) {
-          // records of list b that come first: smaller key, or equal key of a lower atom
-          const int* kb = lk + b * kC;
-          int c = 0;
+    for (int b = 0; b < NB; ++b) cnt[b] = __popcll((m >> (b * kC)) & seg);
+    if (sorted) {
+      // Records of list b that come first: smaller key, or equal key of a
+      // lower atom.  The NB binary searches run side by side without
+      // branches, so each step is one round trip to LDS for all lists.
+      int c[NB];
 #pragma unroll
-          for (int step = kC; step > 0; step >>= 1) {
-            if (c + step <= cnt_b) {
-              const int kk = kb[c + step - 1];
-              if (b < a ? kk <= key : kk < key) c += step;
-            }
-          }
-          r += b == a ? 0 : c;
-        } else {
-          r += b < a ? cnt_b : 0;
+      for (int b = 0; b < NB; ++b) c[b] = 0;
+#pragma unroll
+      for (int step = kC; step > 0; step >>= 1) {
+        int kk[NB];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) kk[b] = lk[b * kC + max(min(c[b] + step, cnt[b]) - 1, 0)];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          const bool lt = b < a ? kk[b] <= key : kk[b] < key;
+          c[b] += (c[b] + step <= cnt[b] && lt) ? step : 0;
         }
       }
+#pragma unroll
+      for (int b = 0; b < NB; ++b) r += b == a ? 0 : c[b];
+    } else {
+#pragma unroll
+      for (int b = 0; b < NB; ++b) r += b < a ? cnt[b] : 0;
     }
   }
   if (valid) {
@@ -434,7 +433,7 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_fwd_kernel(
   unsigned char* wb = smem + zoff;
   WaveLds<TI>& W = *reinterpret_cast<WaveLds<TI>*>(wb);
   const __amdgpu_buffer_rsrc_t rs = make_rsrc(coeff, g.coeff_bytes);
-  const int voff = min(lane * CPL, ld - CPL) * (int)sizeof(TI);
+  const int voff = 2 * min(lane * CPL, ld - CPL) * (int)sizeof(TI);
 
   int ai[NB];
 #pragma unroll
@@ -643,7 +642,7 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
   const unsigned char* const rlane =
       red + (lane >> 4) * 2 * kRedBlock + ((lane >> 3) & 1) * kRedBlock + (lane & 7) * 16;
   const __amdgpu_buffer_rsrc_t rs = make_rsrc(coeff, g.coeff_bytes);
-  const int voff = min(lane * CPL, ld - CPL) * (int)sizeof(TI);
+  const int voff = 2 * min(lane * CPL, ld - CPL) * (int)sizeof(TI);
 
   TA dt[NB][CPL][4];
   int ai[NB];
@@ -810,26 +809,25 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
 //   sum_m dT[m][k] g_m(t)                  = sum_q t^q P[k][q]
 //   sum_m g'_m(t) sum_k' dT[m][k'] R~[k']  = sum_k' R~[k'] sum_q q t^(q-1) P[k'][q].
 // P of each (interval, atom) pair of a chunk set comes from two chains of
-// v_mfma_f64_4x4x4f64 (powers 0-3 and 4-7, of which 6 and 7 are not used),
-// and each record then costs a few dozen operations in the lane that owns
-// its slot.
+// v_mfma_f64_4x4x4f64 (even powers 0, 2, 4, 6 and odd powers 1, 3, 5, 7, of
+// which 6 and 7 are not used), and each record then costs a few dozen
+// operations in the lane that owns its slot.
 //
 // v_mfma_f64_4x4x4f64 computes four independent 4x4 products D_b = A_b B_b
 // (+ C_b).  Lane L = 16 kk + 4 b + x holds A_b[x][kk] and B_b[kk][x]; D_b[i][j]
 // sits in lane 16 i + 4 b + j (measured on gfx950).  Block b is a quarter of
 // the channels, 4S channels each; A_b = dT^T of the quarter (rows k), B_b the
-// quarter's coefficients (columns q).  K step s < 2 (S / 2) of quarter h
-// covers the channels h*4S + 8(s/2) + 2kk + s%2, so that one 16-byte load of
-// a lane brings its coefficients for two consecutive K steps; for odd S the
-// last step covers h*4S + 4(S-1) + kk.  The four quarters' products are summed
-// across lanes (DPP row shifts) into the lanes of quarter 3, which store P.
+// quarter's coefficients (column x of chain c = power 2x + c).  K step s of
+// quarter h covers the channels h*4S + 4s + kk, and one 16-byte read of the
+// power pair (2x, 2x + 1) of a channel gives a lane its B operands of both
+// chains.  The four quarters' products are summed across lanes (DPP row
+// shifts) into the lanes of quarter 3, which store P.
 //
-// The B operands are not loaded from the table directly (two power groups,
-// 8 loads per interval for M1 = 100, a quarter of them repeating power 5):
-// an interval's 6 rows are fetched densely by NS wave-wide 16-byte loads (5
-// for M1 = 100), written to a per-wavefront LDS slot, and read from there.
-// The vector memory address unit, which bounds this kernel, then does 5/8
-// of the work.
+// The B operands are not loaded from the table directly (S loads per interval
+// and lane, 7 for M1 = 100): an interval's 6 ld coefficients are fetched
+// densely by NS wave-wide 16-byte loads (5 for M1 = 100), written to a
+// per-wavefront LDS slot, and read from there.  The vector memory address
+// unit, which bounds this kernel, then does 5/7 of the work.
 constexpr int kMfmaAtoms = 4;      // atoms per wavefront in the matrix-core kernel
 
 // An interval's coefficients (6 rows of ld) are staged in LDS by NS wave-wide
@@ -864,7 +862,6 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
                           const double* __restrict__ em, const double* __restrict__ dT,
                           double* __restrict__ dR) {
   static_assert(S >= 1 && S <= 8, "K steps per channel quarter");
-  constexpr int S2 = S / 2;           // 16-byte loads per chain and interval
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int NB = kMfmaAtoms;
   constexpr int kC = kLanes / NB;
@@ -884,18 +881,11 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
 
   // this lane's place in the MFMA operands: K index kk, block = channel quarter h
   const int kk = lane >> 4, h = (lane >> 2) & 3, x = lane & 3;
-  const int ch0 = h * 4 * S + 2 * kk;                 // channel of K step 0
-  const int chl = h * 4 * S + 4 * (S - 1) + kk;       // channel of the last step, S odd
-  int boff[2], boffl[2];
-#pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    const int q = min(4 * c + x, 5);                  // power held in B (6, 7 repeat 5)
-    boff[c] = (q * ld + ch0) * (int)sizeof(double);    // inside the LDS slot
-    boffl[c] = (q * ld + chl) * (int)sizeof(double);
-  }
-  auto channel = [&](int s) __attribute__((always_inline)) {
-    return s < 2 * S2 ? ch0 + 8 * (s >> 1) + (s & 1) : chl;
-  };
+  // B column x of chain c is the power 2x + c, so that one 16-byte read of a
+  // power pair gives a lane both chains' operands (x = 3 repeats the pair of
+  // powers 4 and 5: those columns are not used)
+  const uint32_t boff = (uint32_t)(min(x, 2) * 2 * ld + 2 * (h * 4 * S + kk)) * sizeof(double);
+  auto channel = [&](int s) __attribute__((always_inline)) { return h * 4 * S + 4 * s + kk; };
 
   // A operands: dT of the wave's atoms, transposed, zero past M1
   double A[NB][S];
@@ -939,17 +929,11 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
   };
   auto read_b = [&](double (&B)[2][S]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-#pragma unroll
-      for (int s2 = 0; s2 < S2; ++s2) {
-        const Pair<double> v = *reinterpret_cast<const Pair<double>*>(
-            __builtin_assume_aligned(smem + slot + boff[c] + 64 * s2, 16));
-        B[c][2 * s2] = v.x;
-        B[c][2 * s2 + 1] = v.y;
-      }
-      if constexpr (S % 2 == 1)
-        B[c][S - 1] = *reinterpret_cast<const double*>(
-            __builtin_assume_aligned(smem + slot + boffl[c], 8));
+    for (int st = 0; st < S; ++st) {      // K step st: channel h*4S + 4 st + kk
+      const Pair<double> v = *reinterpret_cast<const Pair<double>*>(
+          __builtin_assume_aligned(smem + slot + boff + 64 * st, 16));
+      B[0][st] = v.x;
+      B[1][st] = v.y;
     }
   };
   v4i stg[NS];
@@ -1038,10 +1022,9 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
             d1 += row_shr<4>(d1);
             d0 += row_shr<8>(d0);
             d1 += row_shr<8>(d1);
-            if (h == 3) {
-              double* o = store + np * 32 + 8 * kk + x;   // P[k = kk][q]
-              o[0] = d0;
-              o[4] = d1;
+            if (h == 3) {   // P[k = kk][q = 2x + c] (row k is 8 doubles, q = 6, 7 unused)
+              *reinterpret_cast<Pair<double>*>(__builtin_assume_aligned(
+                  store + np * 32 + 8 * kk + 2 * x, 16)) = Pair<double>{d0, d1};
             }
             ++np;
           }

@@ -107,16 +107,16 @@ void fit_segment(const double* y0, const double* y0p, const double* y0pp, const 
     const double a = (6.0 * A - 3.0 * B * dt + 0.5 * C * dt2) / dt5;
     const double b = (-15.0 * A + 7.0 * B * dt - C * dt2) / dt4;
     const double c = (10.0 * A - 4.0 * B * dt + 0.5 * C * dt2) / dt3;
-    // row q holds the coefficient of t^q for all channels
-    out[0 * ld + m] = (T)y0[m];
-    out[1 * ld + m] = (T)y0p[m];
-    out[2 * ld + m] = (T)(0.5 * y0pp[m]);
-    out[3 * ld + m] = (T)c;
-    out[4 * ld + m] = (T)b;
-    out[5 * ld + m] = (T)a;
+    // the coefficients of t^(2j) and t^(2j+1) of one channel are adjacent
+    out[DPC_TABLE_AT(ld, 0, m)] = (T)y0[m];
+    out[DPC_TABLE_AT(ld, 1, m)] = (T)y0p[m];
+    out[DPC_TABLE_AT(ld, 2, m)] = (T)(0.5 * y0pp[m]);
+    out[DPC_TABLE_AT(ld, 3, m)] = (T)c;
+    out[DPC_TABLE_AT(ld, 4, m)] = (T)b;
+    out[DPC_TABLE_AT(ld, 5, m)] = (T)a;
   }
   for (int q = 0; q < 6; ++q)
-    for (int m = m1; m < ld; ++m) out[q * ld + m] = (T)0;
+    for (int m = m1; m < ld; ++m) out[DPC_TABLE_AT(ld, q, m)] = (T)0;
 }
 
 template <typename T>

@@ -70,7 +70,7 @@ def _eval_lib(buf, rng, m1, x):
     """Value/slope/curvature of the library's table at x (test-side Horner)."""
     L1, L2 = rng.L1, rng.L2
     ld = B.table_ld(m1)
-    c = buf[rng.offset:rng.offset + (L1 + L2) * 6 * ld].reshape(L1 + L2, 6, ld)[:, :, :m1]
+    c = B.unpack_table(buf[rng.offset:rng.offset + (L1 + L2) * 6 * ld], L1 + L2, ld)[:, :, :m1]
     c = c.astype(np.float64)
     x_up = rng.lo + L1 * rng.d1
     l = np.where(x < x_up, np.clip(np.floor((x - rng.lo) / rng.d1), 0, L1 - 1),
@@ -102,7 +102,7 @@ def test_build_table_matches_oracle_by_evaluation(seed, widths):
 def test_table_padding_is_zero():
     net = random_net(np.random.default_rng(4), (1, 3, 6, 6))    # m1 = 6 -> rows of 8
     r = P.make_ranges([-0.5], [0.01], [20], [0.1], [2])
-    buf = P.build_tables([net], r, P.DPC_F64).reshape(22, 6, 8)
+    buf = B.unpack_table(P.build_tables([net], r, P.DPC_F64), 22, 8)
     assert np.all(buf[:, :, 6:] == 0) and np.any(buf[:, :, :6] != 0)
 
 
