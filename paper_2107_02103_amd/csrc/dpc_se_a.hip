@@ -119,13 +119,16 @@ __device__ __forceinline__ void locate(const PairRange& P, double x, int& l, dou
   const double x_up = P.lo + (double)P.L1 * P.d1;
   const double x_end = x_up + (double)P.L2 * P.d2;
   clamped = false;
+  // interval by multiplication with the reciprocal stride (uniform, hence
+  // computed once, when all pairs share one table); at a node this may pick
+  // the left piece with t = d1, which agrees with the right one to rounding
   if (x < x_up) {
-    double q = floor((x - P.lo) / P.d1);
+    double q = floor((x - P.lo) * (1.0 / P.d1));
     q = fmin(fmax(q, 0.0), (double)(P.L1 - 1));
     l = (int)q;
     t = x - (P.lo + q * P.d1);
   } else if (x < x_end) {
-    double q = floor((x - x_up) / P.d2);
+    double q = floor((x - x_up) * (1.0 / P.d2));
     q = fmin(fmax(q, 0.0), (double)(P.L2 - 1));
     l = P.L1 + (int)q;
     t = x - (x_up + q * P.d2);
@@ -298,8 +301,9 @@ __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[
     valid = (holder >> (il >> 6)) & 1;
     if (valid) {
       load_row(em + row * 4, rec.r);
-      const int blk = block_of(g, j);
-      const PairRange& P = g.pr[at * g.ntypes + blk];
+      // one type: the pair range is uniform (scalar loads); else per lane
+      const int blk = g.ntypes == 1 ? 0 : block_of(g, j);
+      const PairRange P = g.ntypes == 1 ? g.pr[0] : g.pr[at * g.ntypes + blk];
       int l;
       bool cl;
       locate(P, (double)rec.r[0], l, rec.t, cl);
@@ -320,39 +324,42 @@ __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[
   const int pos = lanes_below(m) - __popcll(m & before_seg);
   int r = pos;
   if constexpr (NB > 1) {
-    int* lk = W.rk;            // free until the run tables are written
-    if (valid) lk[a * kC + pos] = key;
-    wave_sync();
+    // Each atom's list of keys, padded to kC entries with 0xFFFFFFFF (above
+    // every key): every lane writes one entry, and the searches below need
+    // no bounds.  Keys are below 2^31 (block < 8), so key + 1 cannot wrap.
+    uint32_t* lk = reinterpret_cast<uint32_t*>(W.rk);  // free until the run tables are written
     const int cnt_a = __popcll((m >> (a * kC)) & seg);
-    bool bad = false;
-    if (sl + 1 < cnt_a) bad = lk[lane] > lk[lane + 1];
+    lk[a * kC + (valid ? pos : cnt_a + sl - pos)] = valid ? (uint32_t)key : 0xFFFFFFFFu;
+    wave_sync();
+    const bool bad = sl + 1 < kC && lk[lane] > lk[lane + 1];
     const bool sorted = __ballot(bad) == 0;
-    int cnt[NB];
-#pragma unroll
-    for (int b = 0; b < NB; ++b) cnt[b] = __popcll((m >> (b * kC)) & seg);
     if (sorted) {
       // Records of list b that come first: smaller key, or equal key of a
-      // lower atom.  The NB binary searches run side by side without
-      // branches, so each step is one round trip to LDS for all lists.
+      // lower atom, i.e. keys below thr[b].  The NB lower-bound searches run
+      // side by side, one round trip to LDS per step for all lists.
+      uint32_t thr[NB];
       int c[NB];
 #pragma unroll
-      for (int b = 0; b < NB; ++b) c[b] = 0;
-#pragma unroll
-      for (int step = kC; step > 0; step >>= 1) {
-        int kk[NB];
-#pragma unroll
-        for (int b = 0; b < NB; ++b) kk[b] = lk[b * kC + max(min(c[b] + step, cnt[b]) - 1, 0)];
-#pragma unroll
-        for (int b = 0; b < NB; ++b) {
-          const bool lt = b < a ? kk[b] <= key : kk[b] < key;
-          c[b] += (c[b] + step <= cnt[b] && lt) ? step : 0;
-        }
+      for (int b = 0; b < NB; ++b) {
+        thr[b] = (uint32_t)key + (b < a ? 1u : 0u);
+        c[b] = 0;
       }
 #pragma unroll
-      for (int b = 0; b < NB; ++b) r += b == a ? 0 : c[b];
+      for (int step = kC / 2; step > 0; step >>= 1) {
+        uint32_t kk[NB];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) kk[b] = lk[b * kC + c[b] + step - 1];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) c[b] += kk[b] < thr[b] ? step : 0;
+      }
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const uint32_t kk = lk[b * kC + c[b]];
+        r += b == a ? 0 : c[b] + (kk < thr[b] ? 1 : 0);
+      }
     } else {
 #pragma unroll
-      for (int b = 0; b < NB; ++b) r += b < a ? cnt[b] : 0;
+      for (int b = 0; b < NB; ++b) r += b < a ? __popcll((m >> (b * kC)) & seg) : 0;
     }
   }
   if (valid) {
@@ -830,14 +837,23 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
 // unit, which bounds this kernel, then does 5/7 of the work.
 constexpr int kMfmaAtoms = 4;      // atoms per wavefront in the matrix-core kernel
 
-// An interval's coefficients (6 rows of ld) are staged in LDS by NS wave-wide
-// 16-byte loads; (interval, atom) products held in LDS at once: pair_slots.
-// Four wavefronts' LDS stays at or below 53,312 bytes, so that three
-// workgroups share a CU (measured: 53,824 bytes leave room for two).
+// An interval's coefficients (3 power-pair rows of ld channels) are fetched
+// by NS wave-wide 16-byte loads and staged in LDS with rows ldp channels
+// apart, ldp >= ld and ldp = 1 (mod 16): a row then starts 16 bytes past a
+// multiple of 256, so that the 16 lanes (quarter h, column x) of one K index
+// read 16 different 16-byte bank groups (for odd S), where rows of ld = 100
+// channels would put 3 or 4 of them on each.  The (interval, atom) products
+// are stored as rows of 6 doubles, 26 doubles (13 bank groups) apart, so
+// that the records of up to 16 different products read without conflicts;
+// pair_slots of them are held at once.  Four wavefronts' LDS stays at or
+// below 53,312 bytes, so that three workgroups share a CU (measured: 53,824
+// bytes leave room for two).
+constexpr int kPairDoubles = 26;   // one product in LDS: 4 rows of 6 + 2 padding
 __host__ __device__ constexpr int pair_slots(int ns) { return ns <= 5 ? 16 : (ns == 6 ? 12 : 8); }
-__host__ __device__ constexpr size_t bwdm_wave_bytes(int ns) {
-  return align16(sizeof(WaveLds<double>)) + (size_t)pair_slots(ns) * 32 * sizeof(double) +
-         (size_t)ns * 1024;
+__host__ __device__ constexpr int staged_ld(int ld) { return ld + ((17 - (ld & 15)) & 15); }
+__host__ __device__ constexpr size_t bwdm_wave_bytes(int ns, int ld) {
+  return align16(sizeof(WaveLds<double>)) + (size_t)pair_slots(ns) * kPairDoubles * sizeof(double) +
+         (size_t)48 * staged_ld(ld);
 }
 
 __device__ __forceinline__ double mfma4(double a, double b, double c) {
@@ -871,12 +887,13 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
   if (i0 >= g.nloc) return;
   const int nnei = g.nnei, m1 = g.m1, ld = g.ld;
   constexpr int kPairSlots = pair_slots(NS);
-  const uint32_t zoff = __builtin_amdgcn_readfirstlane(wave * (uint32_t)bwdm_wave_bytes(NS));
+  const int ldp = staged_ld(ld);
+  const uint32_t zoff = __builtin_amdgcn_readfirstlane(wave * (uint32_t)bwdm_wave_bytes(NS, ld));
   unsigned char* wb = smem + zoff;
   WaveLds<double>& W = *reinterpret_cast<WaveLds<double>*>(wb);
   double* const store = reinterpret_cast<double*>(wb + align16(sizeof(WaveLds<double>)));
   const uint32_t slot = zoff + (uint32_t)(align16(sizeof(WaveLds<double>)) +
-                                          (size_t)kPairSlots * 32 * sizeof(double));
+                                          (size_t)kPairSlots * kPairDoubles * sizeof(double));
   const __amdgpu_buffer_rsrc_t rs = make_rsrc(coeff, g.coeff_bytes);
 
   // this lane's place in the MFMA operands: K index kk, block = channel quarter h
@@ -884,7 +901,24 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
   // B column x of chain c is the power 2x + c, so that one 16-byte read of a
   // power pair gives a lane both chains' operands (x = 3 repeats the pair of
   // powers 4 and 5: those columns are not used)
-  const uint32_t boff = (uint32_t)(min(x, 2) * 2 * ld + 2 * (h * 4 * S + kk)) * sizeof(double);
+  const uint32_t boff = (uint32_t)(min(x, 2) * ldp + h * 4 * S + kk) * 16u;
+  // where the lane's 16 bytes of staging load i go in the slot: unit u =
+  // 64 i + lane of the interval is row u / ld, channel u % ld; the last load
+  // may run past the 3 rows (those lanes do not write)
+  uint32_t poff[NS];
+#pragma unroll
+  for (int i = 0; i < NS; ++i) {
+    const int u = 64 * i + lane, row = u / ld;
+    poff[i] = (uint32_t)(row * ldp + (u - row * ld)) * 16u;
+  }
+  const bool last_in = 64 * (NS - 1) + lane < 3 * ld;
+  // K steps reach channels past M1 (zero A operands); their B operands come
+  // from the row padding, which is set to zero once (0 * garbage may be NaN)
+  if (lane < 3 * (ldp - ld)) {
+    const int row = lane / (ldp - ld);
+    *reinterpret_cast<v4i*>(__builtin_assume_aligned(
+        smem + slot + (row * ldp + ld + (lane - row * (ldp - ld))) * 16, 16)) = v4i{0, 0, 0, 0};
+  }
   auto channel = [&](int s) __attribute__((always_inline)) { return h * 4 * S + 4 * s + kk; };
 
   // A operands: dT of the wave's atoms, transposed, zero past M1
@@ -913,8 +947,7 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
 
   // An interval's coefficients pass through registers (`stg`, 16 bytes per
   // lane and load, in order) into the wave's LDS slot; the B operands are
-  // read from there.  Past the 6 rows the slot holds whatever follows in the
-  // table (or zeros past its end): finite values met only by zero A operands.
+  // read from there.
   auto fetch = [&](int off, v4i (&stg)[NS]) __attribute__((always_inline)) {
     const int soff = off * (int)sizeof(double);
 #pragma unroll
@@ -924,8 +957,8 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
   auto put = [&](const v4i (&stg)[NS]) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < NS; ++i)
-      *reinterpret_cast<v4i*>(__builtin_assume_aligned(smem + slot + 1024 * i + lane * 16, 16)) =
-          stg[i];
+      if (i + 1 < NS || last_in)
+        *reinterpret_cast<v4i*>(__builtin_assume_aligned(smem + slot + poff[i], 16)) = stg[i];
   };
   auto read_b = [&](double (&B)[2][S]) __attribute__((always_inline)) {
 #pragma unroll
@@ -956,14 +989,14 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
       auto eval = [&](int base, int np) __attribute__((always_inline)) {
         wave_sync();
         if (pair >= base && pair < base + np) {
-          const double* sp = store + (pair - base) * 32;
+          const double* sp = store + (pair - base) * kPairDoubles;
           const Rec<double>& rc = zrec<double>(smem, zoff, tb.rank);
           const double t = rc.t;
           const double r0 = rc.r[0], r1 = rc.r[1], r2 = rc.r[2], r3 = rc.r[3];
           double val[4], der[4];
 #pragma unroll
           for (int k = 0; k < 4; ++k) {
-            const Pair<double>* pk = reinterpret_cast<const Pair<double>*>(sp + 8 * k);
+            const Pair<double>* pk = reinterpret_cast<const Pair<double>*>(sp + 6 * k);
             const Pair<double> c01 = pk[0], c23 = pk[1], c45 = pk[2];
             double v = c45.y, d = c45.y;
             v = fma(v, t, c45.x);
@@ -1022,9 +1055,9 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
             d1 += row_shr<4>(d1);
             d0 += row_shr<8>(d0);
             d1 += row_shr<8>(d1);
-            if (h == 3) {   // P[k = kk][q = 2x + c] (row k is 8 doubles, q = 6, 7 unused)
+            if (h == 3 && x < 3) {   // P[k = kk][q = 2x + c] (row k: 6 doubles)
               *reinterpret_cast<Pair<double>*>(__builtin_assume_aligned(
-                  store + np * 32 + 8 * kk + 2 * x, 16)) = Pair<double>{d0, d1};
+                  store + np * kPairDoubles + 6 * kk + 2 * x, 16)) = Pair<double>{d0, d1};
             }
             ++np;
           }
@@ -1134,18 +1167,19 @@ int launch_fwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
 }
 
 // float64 with M1 <= 128: the matrix-core kernel, ceil(M1 / 16) K steps per
-// channel quarter, an interval staged by ceil((48 ld + 128) / 1024) loads
+// channel quarter, an interval (48 ld bytes) staged by ceil(48 ld / 1024)
+// loads, so that only the last one runs past the interval
 template <int S>
 void launch_mfma_s(hipStream_t s, const Geo& g, dim3 grid, dim3 block, const void* coeff,
                    const int* atype, const int* nlist, const void* em, const void* dT, void* dR) {
-  const int ns = (48 * g.ld + 128 + 1023) / 1024;
+  const int ns = (48 * g.ld + 1023) / 1024;
   auto go = [&](auto kern, size_t wave_bytes) {
     hipLaunchKernelGGL(kern, grid, block, kWaves * wave_bytes, s, g, (const double*)coeff,
                        atype, nlist, (const double*)em, (const double*)dT, (double*)dR);
   };
-  constexpr int lo = (48 * (16 * S - 12) + 128 + 1023) / 1024;   // smallest ld of this S
-  if (ns <= lo) go(se_a_bwd_mfma_kernel<S, lo>, bwdm_wave_bytes(lo));
-  else go(se_a_bwd_mfma_kernel<S, lo + 1>, bwdm_wave_bytes(lo + 1));
+  constexpr int lo = (48 * (16 * S - 12) + 1023) / 1024;   // smallest ld of this S
+  if (ns <= lo) go(se_a_bwd_mfma_kernel<S, lo>, bwdm_wave_bytes(lo, g.ld));
+  else go(se_a_bwd_mfma_kernel<S, lo + 1>, bwdm_wave_bytes(lo + 1, g.ld));
 }
 
 int launch_bwd_mfma(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
