@@ -119,16 +119,13 @@ __device__ __forceinline__ void locate(const PairRange& P, double x, int& l, dou
   const double x_up = P.lo + (double)P.L1 * P.d1;
   const double x_end = x_up + (double)P.L2 * P.d2;
   clamped = false;
-  // interval by multiplication with the reciprocal stride (uniform, hence
-  // computed once, when all pairs share one table); at a node this may pick
-  // the left piece with t = d1, which agrees with the right one to rounding
   if (x < x_up) {
-    double q = floor((x - P.lo) * (1.0 / P.d1));
+    double q = floor((x - P.lo) / P.d1);
     q = fmin(fmax(q, 0.0), (double)(P.L1 - 1));
     l = (int)q;
     t = x - (P.lo + q * P.d1);
   } else if (x < x_end) {
-    double q = floor((x - x_up) * (1.0 / P.d2));
+    double q = floor((x - x_up) / P.d2);
     q = fmin(fmax(q, 0.0), (double)(P.L2 - 1));
     l = P.L1 + (int)q;
     t = x - (x_up + q * P.d2);
@@ -279,7 +276,7 @@ __device__ __forceinline__ void store_row(TA* p, const TA (&v)[4]) {
 // the lane also gets the index of its record's (interval, atom) pair among
 // the chunk set's pairs in merged order (`pair`, -1 without a record), a
 // pair being a maximal group of records with equal key and atom.
-template <typename TI, typename TA, int NB, bool kBwd, bool kPairs = false>
+template <typename TI, typename TA, int NB, bool kBwd, bool kOne, bool kPairs = false>
 __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[NB], int i0,
                                                   int s0, int wbase, uint32_t vm,
                                                   const TI* __restrict__ em, WaveLds<TI>& W,
@@ -301,9 +298,15 @@ __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[
     valid = (holder >> (il >> 6)) & 1;
     if (valid) {
       load_row(em + row * 4, rec.r);
-      // one type: the pair range is uniform (scalar loads); else per lane
-      const int blk = g.ntypes == 1 ? 0 : block_of(g, j);
-      const PairRange P = g.ntypes == 1 ? g.pr[0] : g.pr[at * g.ntypes + blk];
+      // one type (kOne): the pair range is uniform (scalar loads); else per lane
+      int blk = 0;
+      PairRange P;
+      if constexpr (kOne) {
+        P = g.pr[0];
+      } else {
+        blk = block_of(g, j);
+        P = g.pr[at * g.ntypes + blk];
+      }
       int l;
       bool cl;
       locate(P, (double)rec.r[0], l, rec.t, cl);
@@ -422,7 +425,8 @@ __host__ __device__ constexpr size_t fwd_wave_bytes(int m1) {
 template <typename TA>
 using Pair = TA __attribute__((ext_vector_type(2)));
 
-template <typename TI, typename TA, int CPL, int NB>
+// kOne: all atoms and neighbours have one type (one table, no blocks)
+template <typename TI, typename TA, int CPL, int NB, bool kOne>
 // up to 128 channels: registers capped so that 3 wavefronts fit on a SIMD
 __global__ __launch_bounds__(64 * kWaves)
 __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_fwd_kernel(
@@ -480,7 +484,7 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_fwd_kernel(
       wbase = s0 - s0 % (kWindow / NB);
       vm = valid_window<NB>(g, i0, wbase, nlist, lane);
     }
-    const Tables tb = build_chunk_set<TI, TA, NB, false>(g, ai, i0, s0, wbase, vm, em, W, lane);
+    const Tables tb = build_chunk_set<TI, TA, NB, false, kOne>(g, ai, i0, s0, wbase, vm, em, W, lane);
     if (tb.n == 0) continue;
     load_coef<TI, CPL>(rs, key_offset(readlane(tb.vk, 0)), ld, voff, cfA);
     int r = 0;
@@ -624,7 +628,7 @@ __host__ __device__ constexpr size_t bwd_wave_bytes() {
   return align16(sizeof(WaveLds<TI>)) + (size_t)2 * kBatch * kRedBlock;
 }
 
-template <typename TI, typename TA, int CPL, int NB>
+template <typename TI, typename TA, int CPL, int NB, bool kOne>
 // up to 128 channels: registers capped so that 3 wavefronts fit on a SIMD
 __global__ __launch_bounds__(64 * kWaves)
 __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
@@ -713,7 +717,7 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
       wbase = s0 - s0 % (kWindow / NB);
       vm = valid_window<NB>(g, i0, wbase, nlist, lane);
     }
-    const Tables tb = build_chunk_set<TI, TA, NB, true>(g, ai, i0, s0, wbase, vm, em, W, lane);
+    const Tables tb = build_chunk_set<TI, TA, NB, true, kOne>(g, ai, i0, s0, wbase, vm, em, W, lane);
     // Each lane writes the dE/dR~ row of its own slot (zero for padding) after
     // the chunk set's runs: consecutive lanes, consecutive rows, and no store
     // ahead of the coefficient loads whose waits would then include it.
@@ -871,7 +875,7 @@ __device__ __forceinline__ double row_shr(double v) {
 }
 
 // up to 128 channels: registers capped so that 3 wavefronts fit on a SIMD
-template <int S, int NS>
+template <int S, int NS, bool kOne>
 __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(3)))
 void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
                           const int* __restrict__ atype, const int* __restrict__ nlist,
@@ -981,7 +985,7 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
       vm = valid_window<NB>(g, i0, wbase, nlist, lane);
     }
     int pair;
-    const Tables tb = build_chunk_set<double, double, NB, true, true>(g, ai, i0, s0, wbase, vm,
+    const Tables tb = build_chunk_set<double, double, NB, true, kOne, true>(g, ai, i0, s0, wbase, vm,
                                                                       em, W, lane, &pair);
     if (tb.n > 0) {
       // the records of pairs [base, base + np) read their products; each
@@ -1159,9 +1163,9 @@ int launch_fwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
                        (const TI*)em, (TA*)T, (TA*)D);
   };
   switch (channels_per_lane(g.m1)) {
-    case 1: go(se_a_fwd_kernel<TI, TA, 1, NB>); break;
-    case 2: go(se_a_fwd_kernel<TI, TA, 2, NB>); break;
-    default: go(se_a_fwd_kernel<TI, TA, 4, NB>); break;
+    case 1: g.ntypes == 1 ? go(se_a_fwd_kernel<TI, TA, 1, NB, true>) : go(se_a_fwd_kernel<TI, TA, 1, NB, false>); break;
+    case 2: g.ntypes == 1 ? go(se_a_fwd_kernel<TI, TA, 2, NB, true>) : go(se_a_fwd_kernel<TI, TA, 2, NB, false>); break;
+    default: g.ntypes == 1 ? go(se_a_fwd_kernel<TI, TA, 4, NB, true>) : go(se_a_fwd_kernel<TI, TA, 4, NB, false>); break;
   }
   return launch_status();
 }
@@ -1178,8 +1182,13 @@ void launch_mfma_s(hipStream_t s, const Geo& g, dim3 grid, dim3 block, const voi
                        atype, nlist, (const double*)em, (const double*)dT, (double*)dR);
   };
   constexpr int lo = (48 * (16 * S - 12) + 1023) / 1024;   // smallest ld of this S
-  if (ns <= lo) go(se_a_bwd_mfma_kernel<S, lo>, bwdm_wave_bytes(lo, g.ld));
-  else go(se_a_bwd_mfma_kernel<S, lo + 1>, bwdm_wave_bytes(lo + 1, g.ld));
+  if (g.ntypes == 1) {
+    if (ns <= lo) go(se_a_bwd_mfma_kernel<S, lo, true>, bwdm_wave_bytes(lo, g.ld));
+    else go(se_a_bwd_mfma_kernel<S, lo + 1, true>, bwdm_wave_bytes(lo + 1, g.ld));
+  } else {
+    if (ns <= lo) go(se_a_bwd_mfma_kernel<S, lo, false>, bwdm_wave_bytes(lo, g.ld));
+    else go(se_a_bwd_mfma_kernel<S, lo + 1, false>, bwdm_wave_bytes(lo + 1, g.ld));
+  }
 }
 
 int launch_bwd_mfma(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
@@ -1221,9 +1230,9 @@ int launch_bwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
                        (const TI*)em, (const TI*)dT, (TA*)dR);
   };
   switch (cpl) {
-    case 1: go(se_a_bwd_kernel<TI, TA, 1, NB>); break;
-    case 2: go(se_a_bwd_kernel<TI, TA, 2, NB>); break;
-    default: go(se_a_bwd_kernel<TI, TA, 4, NB>); break;
+    case 1: g.ntypes == 1 ? go(se_a_bwd_kernel<TI, TA, 1, NB, true>) : go(se_a_bwd_kernel<TI, TA, 1, NB, false>); break;
+    case 2: g.ntypes == 1 ? go(se_a_bwd_kernel<TI, TA, 2, NB, true>) : go(se_a_bwd_kernel<TI, TA, 2, NB, false>); break;
+    default: g.ntypes == 1 ? go(se_a_bwd_kernel<TI, TA, 4, NB, true>) : go(se_a_bwd_kernel<TI, TA, 4, NB, false>); break;
   }
   return launch_status();
 }
