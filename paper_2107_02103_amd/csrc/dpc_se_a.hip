@@ -116,23 +116,20 @@ __device__ __forceinline__ int key_offset(int key) { return kOffMask - (key & kO
 // Interval of x in one pair's table (see dpc_range in dpc.h).  Always float64.
 __device__ __forceinline__ void locate(const PairRange& P, double x, int& l, double& t,
                                        bool& clamped) {
+  // one division: origin, stride and last index of the part (main range or
+  // band) that x falls in are selected first, so lanes do not diverge
   const double x_up = P.lo + (double)P.L1 * P.d1;
   const double x_end = x_up + (double)P.L2 * P.d2;
-  clamped = false;
-  if (x < x_up) {
-    double q = floor((x - P.lo) / P.d1);
-    q = fmin(fmax(q, 0.0), (double)(P.L1 - 1));
-    l = (int)q;
-    t = x - (P.lo + q * P.d1);
-  } else if (x < x_end) {
-    double q = floor((x - x_up) / P.d2);
-    q = fmin(fmax(q, 0.0), (double)(P.L2 - 1));
-    l = P.L1 + (int)q;
-    t = x - (x_up + q * P.d2);
-  } else {
+  const bool main = x < x_up;
+  const double org = main ? P.lo : x_up, d = main ? P.d1 : P.d2;
+  double q = floor((x - org) / d);
+  q = fmin(fmax(q, 0.0), (double)((main ? P.L1 : P.L2) - 1));
+  l = (main ? 0 : P.L1) + (int)q;
+  t = x - (org + q * d);
+  clamped = !(x < x_end);
+  if (clamped) {
     l = P.L1 + P.L2 - 1;
     t = P.d2;
-    clamped = true;
   }
 }
 
@@ -242,6 +239,27 @@ __device__ __forceinline__ uint32_t valid_window(const Geo& g, int i0, int wbase
   return vm;
 }
 
+// Chunk sets of a window that hold at least one valid slot (bit c: chunk set
+// c of the window's 32).  Bit k of lane l covers window index l + 64 k, i.e.
+// atom k / (32 / NB) and chunk set NB (k mod 32 / NB) + l / (64 / NB); the
+// atoms are folded first, then one ballot per remaining bit.
+template <int NB>
+__device__ __forceinline__ uint32_t occupied_chunks(uint32_t vm) {
+  constexpr int B = 32 / NB, kC = kLanes / NB;
+  constexpr uint64_t seg = kC == 64 ? ~0ull : ((1ull << kC) - 1);
+  uint32_t v = 0;
+#pragma unroll
+  for (int a = 0; a < NB; ++a) v |= vm >> (a * B);
+  uint32_t occ = 0;
+#pragma unroll
+  for (int b = 0; b < B; ++b) {
+    const uint64_t bal = __ballot((v >> b) & 1);
+#pragma unroll
+    for (int c = 0; c < NB; ++c) occ |= ((bal >> (c * kC)) & seg) != 0 ? 1u << (NB * b + c) : 0u;
+  }
+  return occ;
+}
+
 // One R~ row (16-byte aligned: checked on the host).
 template <typename TI>
 __device__ __forceinline__ void load_row(const TI* p, TI (&r)[4]) {
@@ -267,6 +285,23 @@ __device__ __forceinline__ void store_row(TA* p, const TA (&v)[4]) {
   } else {
     typedef TA V4 __attribute__((ext_vector_type(4)));
     __builtin_nontemporal_store(V4{v[0], v[1], v[2], v[3]}, reinterpret_cast<V4*>(p));
+  }
+}
+
+// Zero dE/dR~ rows of a chunk set without valid slots (slots s0 + lane % kC
+// of atom lane / kC; atoms past nloc or of an invalid type are skipped).
+template <typename TA, int NB>
+__device__ __forceinline__ void zero_rows(const Geo& g, const int (&ai)[NB], int i0, int s0,
+                                          TA* __restrict__ dR, int lane) {
+  constexpr int kC = kLanes / NB;
+  const int a = lane / kC, j = s0 + lane % kC;
+  int at = -1;
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+    if (b == a) at = ai[b];
+  if (at >= 0 && j < g.nnei) {
+    const TA z[4] = {(TA)0, (TA)0, (TA)0, (TA)0};
+    store_row(dR + ((size_t)(i0 + a) * g.nnei + j) * 4, z);
   }
 }
 
@@ -478,12 +513,14 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_fwd_kernel(
   // latency-bound phase) at the same time.
   const int nch = (nnei + kC - 1) / kC;
   int s0 = ((int)(blockIdx.x * 5 + wave * 3) % nch) * kC;
-  uint32_t vm = 0;
+  uint32_t vm = 0, occ = 0;
   for (int cc = 0, wbase = -1; cc < nch; ++cc, s0 = s0 + kC < nnei ? s0 + kC : 0) {
     if (s0 - s0 % (kWindow / NB) != wbase) {  // window of nlist signs holding s0
       wbase = s0 - s0 % (kWindow / NB);
       vm = valid_window<NB>(g, i0, wbase, nlist, lane);
+      occ = occupied_chunks<NB>(vm);
     }
+    if (!((occ >> ((s0 - wbase) / kC)) & 1)) continue;   // padding only
     const Tables tb = build_chunk_set<TI, TA, NB, false, kOne>(g, ai, i0, s0, wbase, vm, em, W, lane);
     if (tb.n == 0) continue;
     load_coef<TI, CPL>(rs, key_offset(readlane(tb.vk, 0)), ld, voff, cfA);
@@ -711,11 +748,16 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
   // latency-bound phase) at the same time.
   const int nch = (nnei + kC - 1) / kC;
   int s0 = ((int)(blockIdx.x * 5 + wave * 3) % nch) * kC;
-  uint32_t vm = 0;
+  uint32_t vm = 0, occ = 0;
   for (int cc = 0, wbase = -1; cc < nch; ++cc, s0 = s0 + kC < nnei ? s0 + kC : 0) {
     if (s0 - s0 % (kWindow / NB) != wbase) {  // window of nlist signs holding s0
       wbase = s0 - s0 % (kWindow / NB);
       vm = valid_window<NB>(g, i0, wbase, nlist, lane);
+      occ = occupied_chunks<NB>(vm);
+    }
+    if (!((occ >> ((s0 - wbase) / kC)) & 1)) {   // padding only: zero rows
+      zero_rows<TA, NB>(g, ai, i0, s0, dR, lane);
+      continue;
     }
     const Tables tb = build_chunk_set<TI, TA, NB, true, kOne>(g, ai, i0, s0, wbase, vm, em, W, lane);
     // Each lane writes the dE/dR~ row of its own slot (zero for padding) after
@@ -978,11 +1020,16 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
 
   const int nch = (nnei + kC - 1) / kC;
   int s0 = ((int)(blockIdx.x * 5 + wave * 3) % nch) * kC;
-  uint32_t vm = 0;
+  uint32_t vm = 0, occ = 0;
   for (int cc = 0, wbase = -1; cc < nch; ++cc, s0 = s0 + kC < nnei ? s0 + kC : 0) {
     if (s0 - s0 % (kWindow / NB) != wbase) {  // window of nlist signs holding s0
       wbase = s0 - s0 % (kWindow / NB);
       vm = valid_window<NB>(g, i0, wbase, nlist, lane);
+      occ = occupied_chunks<NB>(vm);
+    }
+    if (!((occ >> ((s0 - wbase) / kC)) & 1)) {   // padding only: zero rows
+      zero_rows<double, NB>(g, ai, i0, s0, dR, lane);
+      continue;
     }
     int pair;
     const Tables tb = build_chunk_set<double, double, NB, true, kOne, true>(g, ai, i0, s0, wbase, vm,
