@@ -75,9 +75,9 @@ struct Geo {
 
 template <typename TI>
 struct alignas(16) Rec {       // one valid neighbour, as staged in LDS
+  double t;                    // offset from the left node of its interval (read first:
+  double pad;                  //   the polynomial needs it before the row)
   TI r[4];                     // its row of R~ (zero in the backward pass when clamped)
-  double t;                    // offset from the left node of its interval
-  double pad;
 };
 
 // LDS of one wavefront for one chunk set.
