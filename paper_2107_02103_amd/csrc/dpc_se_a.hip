@@ -80,14 +80,19 @@ struct alignas(16) Rec {       // one valid neighbour, as staged in LDS
   TI r[4];                     // its row of R~ (zero in the backward pass when clamped)
 };
 
-// LDS of one wavefront for one chunk set.
-template <typename TI>
-struct WaveLds {
-  Rec<TI> z[kLanes];           // merged records
+// A chunk set's keys and run tables in LDS (dead while its runs are walked).
+struct ChunkScratch {
   int mk[kLanes];              // keys in merged order
   int mi[kLanes];              // slot | atom << 20 in merged order
   int rk[kLanes + 2];          // run keys (before that: keys of the compacted per-atom lists)
   int rs[kLanes + 2];          // run starts, then the record count
+};
+
+// LDS of one wavefront for one chunk set.
+template <typename TI>
+struct WaveLds {
+  Rec<TI> z[kLanes];           // merged records
+  ChunkScratch s;
 };
 
 __host__ __device__ constexpr size_t align16(size_t x) { return (x + 15) & ~size_t(15); }
@@ -314,8 +319,9 @@ __device__ __forceinline__ void zero_rows(const Geo& g, const int (&ai)[NB], int
 template <typename TI, typename TA, int NB, bool kBwd, bool kOne, bool kPairs = false>
 __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[NB], int i0,
                                                   int s0, int wbase, uint32_t vm,
-                                                  const TI* __restrict__ em, WaveLds<TI>& W,
-                                                  int lane, int* pair = nullptr) {
+                                                  const TI* __restrict__ em, Rec<TI>* z,
+                                                  ChunkScratch& W, int lane,
+                                                  int* pair = nullptr) {
   constexpr int kC = kLanes / NB;
   const int a = lane / kC, sl = lane % kC, j = s0 + sl;
   int at = -1;
@@ -401,7 +407,7 @@ __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[
     }
   }
   if (valid) {
-    W.z[r] = rec;
+    z[r] = rec;
     W.mk[r] = key;
     W.mi[r] = j | (a << 20);
   }
@@ -521,7 +527,7 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_fwd_kernel(
       occ = occupied_chunks<NB>(vm);
     }
     if (!((occ >> ((s0 - wbase) / kC)) & 1)) continue;   // padding only
-    const Tables tb = build_chunk_set<TI, TA, NB, false, kOne>(g, ai, i0, s0, wbase, vm, em, W, lane);
+    const Tables tb = build_chunk_set<TI, TA, NB, false, kOne>(g, ai, i0, s0, wbase, vm, em, W.z, W.s, lane);
     if (tb.n == 0) continue;
     load_coef<TI, CPL>(rs, key_offset(readlane(tb.vk, 0)), ld, voff, cfA);
     int r = 0;
@@ -759,7 +765,7 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
       zero_rows<TA, NB>(g, ai, i0, s0, dR, lane);
       continue;
     }
-    const Tables tb = build_chunk_set<TI, TA, NB, true, kOne>(g, ai, i0, s0, wbase, vm, em, W, lane);
+    const Tables tb = build_chunk_set<TI, TA, NB, true, kOne>(g, ai, i0, s0, wbase, vm, em, W.z, W.s, lane);
     // Each lane writes the dE/dR~ row of its own slot (zero for padding) after
     // the chunk set's runs: consecutive lanes, consecutive rows, and no store
     // ahead of the coefficient loads whose waits would then include it.
@@ -1033,7 +1039,7 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
     }
     int pair;
     const Tables tb = build_chunk_set<double, double, NB, true, kOne, true>(g, ai, i0, s0, wbase, vm,
-                                                                      em, W, lane, &pair);
+                                                                      em, W.z, W.s, lane, &pair);
     if (tb.n > 0) {
       // the records of pairs [base, base + np) read their products; each
       // result replaces its record in LDS
