@@ -315,13 +315,14 @@ __device__ __forceinline__ void zero_rows(const Geo& g, const int (&ai)[NB], int
 // the backward pass (kBwd) clamped records get a zero R~ row.  With kPairs
 // the lane also gets the index of its record's (interval, atom) pair among
 // the chunk set's pairs in merged order (`pair`, -1 without a record), a
-// pair being a maximal group of records with equal key and atom.
+// pair being a maximal group of records with equal key and atom, and keeps
+// its record in registers (`mine`) instead of writing it to z.
 template <typename TI, typename TA, int NB, bool kBwd, bool kOne, bool kPairs = false>
 __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[NB], int i0,
                                                   int s0, int wbase, uint32_t vm,
                                                   const TI* __restrict__ em, Rec<TI>* z,
                                                   ChunkScratch& W, int lane,
-                                                  int* pair = nullptr) {
+                                                  int* pair = nullptr, Rec<TI>* mine = nullptr) {
   constexpr int kC = kLanes / NB;
   const int a = lane / kC, sl = lane % kC, j = s0 + sl;
   int at = -1;
@@ -333,6 +334,7 @@ __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[
   const int holder = __builtin_amdgcn_ds_bpermute((il & 63) << 2, (int)vm);
   bool valid = false;
   Rec<TI> rec;
+  if constexpr (kPairs) rec = Rec<TI>{0.0, 0.0, {(TI)0, (TI)0, (TI)0, (TI)0}};
   int key = 0;
   if (at >= 0 && j < g.nnei) {
     const size_t row = (size_t)(i0 + a) * g.nnei + j;
@@ -406,8 +408,9 @@ __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[
       for (int b = 0; b < NB; ++b) r += b < a ? __popcll((m >> (b * kC)) & seg) : 0;
     }
   }
+  if constexpr (kPairs) *mine = rec;
   if (valid) {
-    z[r] = rec;
+    if constexpr (!kPairs) z[r] = rec;
     W.mk[r] = key;
     W.mi[r] = j | (a << 20);
   }
@@ -870,42 +873,52 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
 // P of each (interval, atom) pair of a chunk set comes from two chains of
 // v_mfma_f64_4x4x4f64 (even powers 0, 2, 4, 6 and odd powers 1, 3, 5, 7, of
 // which 6 and 7 are not used), and each record then costs a few dozen
-// operations in the lane that owns its slot.
+// operations in the lane that holds it.
 //
 // v_mfma_f64_4x4x4f64 computes four independent 4x4 products D_b = A_b B_b
 // (+ C_b).  Lane L = 16 kk + 4 b + x holds A_b[x][kk] and B_b[kk][x]; D_b[i][j]
-// sits in lane 16 i + 4 b + j (measured on gfx950).  Block b is a quarter of
-// the channels, 4S channels each; A_b = dT^T of the quarter (rows k), B_b the
-// quarter's coefficients (column x of chain c = power 2x + c).  K step s of
-// quarter h covers the channels h*4S + 4s + kk, and one 16-byte read of the
-// power pair (2x, 2x + 1) of a channel gives a lane its B operands of both
-// chains.  The four quarters' products are summed across lanes (DPP row
-// shifts) into the lanes of quarter 3, which store P.
+// sits in lane 16 i + 4 b + j (measured on gfx950).  Block b = h takes the
+// channels m = h (mod 4); A_b = dT^T of those channels (rows k), B_b their
+// coefficients (column x of chain c = power 2x + c).  K step s of block h
+// covers the channels 16 s + 4 kk + h, and one 16-byte read of the power pair
+// (2x, 2x + 1) of a channel gives a lane its B operands of both chains.  The
+// four blocks' products are summed across lanes (DPP row shifts) into the
+// lanes of block 3, which store P.
 //
 // The B operands are not loaded from the table directly (S loads per interval
-// and lane, 7 for M1 = 100): an interval's 6 ld coefficients are fetched
-// densely by NS wave-wide 16-byte loads (5 for M1 = 100), written to a
-// per-wavefront LDS slot, and read from there.  The vector memory address
-// unit, which bounds this kernel, then does 5/7 of the work.
+// and lane, 7 for M1 = 100): an interval's coefficients are copied densely
+// into a per-wavefront LDS slot by NS wave-wide 16-byte buffer loads that
+// write LDS themselves (5 for M1 = 100), and read from there.  The vector
+// memory address unit then does 5/7 of the work, and the copy takes neither
+// registers nor LDS write instructions.  In a slot, row x (power pair x)
+// starts 16 ld bytes after row x - 1; the 16 lanes of one K index kk read the
+// channels 16 s + 4 kk + h of rows x = 0..2, i.e. 16-byte bank groups
+// 4 x + h + const (mod 16) when ld = 4 (mod 16) (M1 = 100: ld = 100), which
+// are distinct.  Reads past channel M1 (zero A operands) fall into the next
+// row or past the interval, inside the slot.
 constexpr int kMfmaAtoms = 4;      // atoms per wavefront in the matrix-core kernel
 
-// An interval's coefficients (3 power-pair rows of ld channels) are fetched
-// by NS wave-wide 16-byte loads and staged in LDS with rows ldp channels
-// apart, ldp >= ld and ldp = 1 (mod 16): a row then starts 16 bytes past a
-// multiple of 256, so that the 16 lanes (quarter h, column x) of one K index
-// read 16 different 16-byte bank groups (for odd S), where rows of ld = 100
-// channels would put 3 or 4 of them on each.  The (interval, atom) products
-// are stored as rows of 6 doubles, 26 doubles (13 bank groups) apart, so
-// that the records of up to 16 different products read without conflicts;
-// pair_slots of them are held at once.  Four wavefronts' LDS stays at or
-// below 53,312 bytes, so that three workgroups share a CU (measured: 53,824
-// bytes leave room for two).
+// 16-byte loads that copy one interval: its 48 ld bytes and the reads of the
+// last K step (up to channel 16 S - 1 of row 2) fit in NS KiB.
+__host__ __device__ constexpr int mfma_slot_kib(int S, int ld) { return (2 * ld + 16 * S + 63) / 64; }
+
+// The (interval, atom) products are stored as rows of 6 doubles, 26 doubles
+// (13 bank groups) apart, so that the records of up to 16 different products
+// read without conflicts; pair_slots of them are held at once.  Four
+// wavefronts' LDS stays at or below 53,312 bytes, so that three workgroups
+// share a CU (measured: 53,824 bytes leave room for two).
 constexpr int kPairDoubles = 26;   // one product in LDS: 4 rows of 6 + 2 padding
-__host__ __device__ constexpr int pair_slots(int ns) { return ns <= 5 ? 16 : (ns == 6 ? 12 : 8); }
-__host__ __device__ constexpr int staged_ld(int ld) { return ld + ((17 - (ld & 15)) & 15); }
-__host__ __device__ constexpr size_t bwdm_wave_bytes(int ns, int ld) {
-  return align16(sizeof(WaveLds<double>)) + (size_t)pair_slots(ns) * kPairDoubles * sizeof(double) +
-         (size_t)48 * staged_ld(ld);
+constexpr int kMfmaWaveLds = 53312 / kWaves;
+__host__ __device__ constexpr int pair_slots(int ns) {
+  return ((kMfmaWaveLds - (int)align16(sizeof(ChunkScratch)) - 1024 * ns) /
+              (kPairDoubles * (int)sizeof(double)) / 4 * 4 > 32
+              ? 32
+              : (kMfmaWaveLds - (int)align16(sizeof(ChunkScratch)) - 1024 * ns) /
+                    (kPairDoubles * (int)sizeof(double)) / 4 * 4);
+}
+__host__ __device__ constexpr size_t bwdm_wave_bytes(int ns) {
+  return align16(sizeof(ChunkScratch)) + (size_t)pair_slots(ns) * kPairDoubles * sizeof(double) +
+         (size_t)1024 * ns;
 }
 
 __device__ __forceinline__ double mfma4(double a, double b, double c) {
@@ -922,6 +935,80 @@ __device__ __forceinline__ double row_shr(double v) {
   return __builtin_bit_cast(double, r);
 }
 
+// The slot is written by buffer loads (counted in vmcnt) that the compiler
+// does not order against LDS instructions it emits itself: it would wait for
+// all of them before every LDS access.  Inside the run loop all LDS accesses
+// are therefore written out here, each block ending in its own lgkmcnt(0),
+// and the loop waits for the copy explicitly.
+__device__ __forceinline__ uint32_t lds_addr(const unsigned char* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) unsigned char*)p;
+}
+
+// q[st] = 16 bytes at a + 256 st (S reads)
+template <int S>
+__device__ __forceinline__ void lds_read_steps(uint32_t a, v4i (&q)[S]) {
+  static_assert(S >= 1 && S <= 8, "K steps");
+#define DPC_R(i, off) "ds_read_b128 %" #i ", %[a] offset:" #off "\n\t"
+  if constexpr (S == 1)
+    asm volatile(DPC_R(0, 0) "s_waitcnt lgkmcnt(0)" : "=&v"(q[0]) : [a] "v"(a) : "memory");
+  else if constexpr (S == 2)
+    asm volatile(DPC_R(0, 0) DPC_R(1, 256) "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(q[0]), "=&v"(q[1]) : [a] "v"(a) : "memory");
+  else if constexpr (S == 3)
+    asm volatile(DPC_R(0, 0) DPC_R(1, 256) DPC_R(2, 512) "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(q[0]), "=&v"(q[1]), "=&v"(q[2]) : [a] "v"(a) : "memory");
+  else if constexpr (S == 4)
+    asm volatile(DPC_R(0, 0) DPC_R(1, 256) DPC_R(2, 512) DPC_R(3, 768) "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(q[0]), "=&v"(q[1]), "=&v"(q[2]), "=&v"(q[3]) : [a] "v"(a) : "memory");
+  else if constexpr (S == 5)
+    asm volatile(DPC_R(0, 0) DPC_R(1, 256) DPC_R(2, 512) DPC_R(3, 768) DPC_R(4, 1024) "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(q[0]), "=&v"(q[1]), "=&v"(q[2]), "=&v"(q[3]), "=&v"(q[4])
+                 : [a] "v"(a) : "memory");
+  else if constexpr (S == 6)
+    asm volatile(DPC_R(0, 0) DPC_R(1, 256) DPC_R(2, 512) DPC_R(3, 768) DPC_R(4, 1024) DPC_R(5, 1280) "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(q[0]), "=&v"(q[1]), "=&v"(q[2]), "=&v"(q[3]), "=&v"(q[4]), "=&v"(q[5])
+                 : [a] "v"(a) : "memory");
+  else if constexpr (S == 7)
+    asm volatile(DPC_R(0, 0) DPC_R(1, 256) DPC_R(2, 512) DPC_R(3, 768) DPC_R(4, 1024) DPC_R(5, 1280) DPC_R(6, 1536)
+                 "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(q[0]), "=&v"(q[1]), "=&v"(q[2]), "=&v"(q[3]), "=&v"(q[4]), "=&v"(q[5]),
+                   "=&v"(q[6])
+                 : [a] "v"(a) : "memory");
+  else
+    asm volatile(DPC_R(0, 0) DPC_R(1, 256) DPC_R(2, 512) DPC_R(3, 768) DPC_R(4, 1024) DPC_R(5, 1280) DPC_R(6, 1536) DPC_R(7, 1792)
+                 "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(q[0]), "=&v"(q[1]), "=&v"(q[2]), "=&v"(q[3]), "=&v"(q[4]), "=&v"(q[5]),
+                   "=&v"(q[6]), "=&v"(q[7])
+                 : [a] "v"(a) : "memory");
+#undef DPC_R
+}
+
+// One product, 4 rows of 6 doubles at a (12 reads of 16 bytes).
+__device__ __forceinline__ void lds_read_pair(uint32_t a, v4i (&q)[12]) {
+  asm volatile(
+      "ds_read_b128 %0, %[a]\n\tds_read_b128 %1, %[a] offset:16\n\t"
+      "ds_read_b128 %2, %[a] offset:32\n\tds_read_b128 %3, %[a] offset:48\n\t"
+      "ds_read_b128 %4, %[a] offset:64\n\tds_read_b128 %5, %[a] offset:80\n\t"
+      "ds_read_b128 %6, %[a] offset:96\n\tds_read_b128 %7, %[a] offset:112\n\t"
+      "ds_read_b128 %8, %[a] offset:128\n\tds_read_b128 %9, %[a] offset:144\n\t"
+      "ds_read_b128 %10, %[a] offset:160\n\tds_read_b128 %11, %[a] offset:176\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(q[0]), "=&v"(q[1]), "=&v"(q[2]), "=&v"(q[3]), "=&v"(q[4]), "=&v"(q[5]),
+        "=&v"(q[6]), "=&v"(q[7]), "=&v"(q[8]), "=&v"(q[9]), "=&v"(q[10]), "=&v"(q[11])
+      : [a] "v"(a)
+      : "memory");
+}
+
+__device__ __forceinline__ void lds_write16(uint32_t a, v4i v) {
+  asm volatile("ds_write_b128 %0, %1" : : "v"(a), "v"(v) : "memory");
+}
+
+// vmcnt(0) only; the empty asm keeps memory accesses on their side of it
+__device__ __forceinline__ void wait_copies() {
+  __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (15 << 8));
+  __asm__ __volatile__("" ::: "memory");
+}
+
 // up to 128 channels: registers capped so that 3 wavefronts fit on a SIMD
 template <int S, int NS, bool kOne>
 __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(3)))
@@ -929,7 +1016,7 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
                           const int* __restrict__ atype, const int* __restrict__ nlist,
                           const double* __restrict__ em, const double* __restrict__ dT,
                           double* __restrict__ dR) {
-  static_assert(S >= 1 && S <= 8, "K steps per channel quarter");
+  static_assert(S >= 1 && S <= 8, "K steps per channel block");
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int NB = kMfmaAtoms;
   constexpr int kC = kLanes / NB;
@@ -939,39 +1026,20 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
   if (i0 >= g.nloc) return;
   const int nnei = g.nnei, m1 = g.m1, ld = g.ld;
   constexpr int kPairSlots = pair_slots(NS);
-  const int ldp = staged_ld(ld);
-  const uint32_t zoff = __builtin_amdgcn_readfirstlane(wave * (uint32_t)bwdm_wave_bytes(NS, ld));
-  unsigned char* wb = smem + zoff;
-  WaveLds<double>& W = *reinterpret_cast<WaveLds<double>*>(wb);
-  double* const store = reinterpret_cast<double*>(wb + align16(sizeof(WaveLds<double>)));
-  const uint32_t slot = zoff + (uint32_t)(align16(sizeof(WaveLds<double>)) +
-                                          (size_t)kPairSlots * kPairDoubles * sizeof(double));
+  const uint32_t zoff = __builtin_amdgcn_readfirstlane(wave * (uint32_t)bwdm_wave_bytes(NS));
+  ChunkScratch& W = *reinterpret_cast<ChunkScratch*>(smem + zoff);
+  const uint32_t store = lds_addr(smem) + zoff + (uint32_t)align16(sizeof(ChunkScratch));
+  unsigned char* const slot_p =
+      smem + zoff + align16(sizeof(ChunkScratch)) + (size_t)kPairSlots * kPairDoubles * sizeof(double);
   const __amdgpu_buffer_rsrc_t rs = make_rsrc(coeff, g.coeff_bytes);
 
-  // this lane's place in the MFMA operands: K index kk, block = channel quarter h
+  // this lane's place in the MFMA operands: K index kk, block h, column x
   const int kk = lane >> 4, h = (lane >> 2) & 3, x = lane & 3;
   // B column x of chain c is the power 2x + c, so that one 16-byte read of a
   // power pair gives a lane both chains' operands (x = 3 repeats the pair of
   // powers 4 and 5: those columns are not used)
-  const uint32_t boff = (uint32_t)(min(x, 2) * ldp + h * 4 * S + kk) * 16u;
-  // where the lane's 16 bytes of staging load i go in the slot: unit u =
-  // 64 i + lane of the interval is row u / ld, channel u % ld; the last load
-  // may run past the 3 rows (those lanes do not write)
-  uint32_t poff[NS];
-#pragma unroll
-  for (int i = 0; i < NS; ++i) {
-    const int u = 64 * i + lane, row = u / ld;
-    poff[i] = (uint32_t)(row * ldp + (u - row * ld)) * 16u;
-  }
-  const bool last_in = 64 * (NS - 1) + lane < 3 * ld;
-  // K steps reach channels past M1 (zero A operands); their B operands come
-  // from the row padding, which is set to zero once (0 * garbage may be NaN)
-  if (lane < 3 * (ldp - ld)) {
-    const int row = lane / (ldp - ld);
-    *reinterpret_cast<v4i*>(__builtin_assume_aligned(
-        smem + slot + (row * ldp + ld + (lane - row * (ldp - ld))) * 16, 16)) = v4i{0, 0, 0, 0};
-  }
-  auto channel = [&](int s) __attribute__((always_inline)) { return h * 4 * S + 4 * s + kk; };
+  const uint32_t bread = lds_addr(slot_p) + (uint32_t)(min(x, 2) * ld + 4 * kk + h) * 16u;
+  auto channel = [&](int s) __attribute__((always_inline)) { return 16 * s + 4 * kk + h; };
 
   // A operands: dT of the wave's atoms, transposed, zero past M1
   double A[NB][S];
@@ -997,32 +1065,15 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
     }
   }
 
-  // An interval's coefficients pass through registers (`stg`, 16 bytes per
-  // lane and load, in order) into the wave's LDS slot; the B operands are
-  // read from there.
-  auto fetch = [&](int off, v4i (&stg)[NS]) __attribute__((always_inline)) {
+  // copy the interval whose coefficients start at element `off` into the slot
+  auto fetch = [&](int off) __attribute__((always_inline)) {
     const int soff = off * (int)sizeof(double);
 #pragma unroll
     for (int i = 0; i < NS; ++i)
-      stg[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, lane * 16, soff + 1024 * i, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rs, (__attribute__((address_space(3))) void*)(slot_p + 1024 * i), 16, lane * 16,
+          soff + 1024 * i, 0, 0);
   };
-  auto put = [&](const v4i (&stg)[NS]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < NS; ++i)
-      if (i + 1 < NS || last_in)
-        *reinterpret_cast<v4i*>(__builtin_assume_aligned(smem + slot + poff[i], 16)) = stg[i];
-  };
-  auto read_b = [&](double (&B)[2][S]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int st = 0; st < S; ++st) {      // K step st: channel h*4S + 4 st + kk
-      const Pair<double> v = *reinterpret_cast<const Pair<double>*>(
-          __builtin_assume_aligned(smem + slot + boff + 64 * st, 16));
-      B[0][st] = v.x;
-      B[1][st] = v.y;
-    }
-  };
-  v4i stg[NS];
-  double Bc[2][S];
 
   const int nch = (nnei + kC - 1) / kC;
   int s0 = ((int)(blockIdx.x * 5 + wave * 3) % nch) * kC;
@@ -1038,23 +1089,23 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
       continue;
     }
     int pair;
-    const Tables tb = build_chunk_set<double, double, NB, true, kOne, true>(g, ai, i0, s0, wbase, vm,
-                                                                      em, W.z, W.s, lane, &pair);
+    Rec<double> mine;
+    const Tables tb = build_chunk_set<double, double, NB, true, kOne, true>(
+        g, ai, i0, s0, wbase, vm, em, nullptr, W, lane, &pair, &mine);
+    double out[4] = {0.0, 0.0, 0.0, 0.0};   // this lane's dE/dR~ row
     if (tb.n > 0) {
-      // the records of pairs [base, base + np) read their products; each
-      // result replaces its record in LDS
+      // the lanes whose records belong to pairs [base, base + np) read their products
       auto eval = [&](int base, int np) __attribute__((always_inline)) {
-        wave_sync();
         if (pair >= base && pair < base + np) {
-          const double* sp = store + (pair - base) * kPairDoubles;
-          const Rec<double>& rc = zrec<double>(smem, zoff, tb.rank);
-          const double t = rc.t;
-          const double r0 = rc.r[0], r1 = rc.r[1], r2 = rc.r[2], r3 = rc.r[3];
+          v4i q[12];
+          lds_read_pair(store + (uint32_t)((pair - base) * kPairDoubles * sizeof(double)), q);
+          const double t = mine.t;
           double val[4], der[4];
 #pragma unroll
           for (int k = 0; k < 4; ++k) {
-            const Pair<double>* pk = reinterpret_cast<const Pair<double>*>(sp + 6 * k);
-            const Pair<double> c01 = pk[0], c23 = pk[1], c45 = pk[2];
+            const Pair<double> c01 = __builtin_bit_cast(Pair<double>, q[3 * k]);
+            const Pair<double> c23 = __builtin_bit_cast(Pair<double>, q[3 * k + 1]);
+            const Pair<double> c45 = __builtin_bit_cast(Pair<double>, q[3 * k + 2]);
             double v = c45.y, d = c45.y;
             v = fma(v, t, c45.x);
             d = fma(d, t, v);
@@ -1068,29 +1119,37 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
             der[k] = d;
           }
           // clamped records carry a zero row, which removes the derivative term
-          double o0 = fma(r0, der[0], val[0]);
-          o0 = fma(r1, der[1], o0);
-          o0 = fma(r2, der[2], o0);
-          o0 = fma(r3, der[3], o0);
-          Pair<double>* o = reinterpret_cast<Pair<double>*>(
-              __builtin_assume_aligned(smem + zoff + tb.rank * (int)sizeof(Rec<double>), 16));
-          o[0] = Pair<double>{o0, val[1]};
-          o[1] = Pair<double>{val[2], val[3]};
+          double o0 = fma(mine.r[0], der[0], val[0]);
+          o0 = fma(mine.r[1], der[1], o0);
+          o0 = fma(mine.r[2], der[2], o0);
+          out[0] = fma(mine.r[3], der[3], o0);
+          out[1] = val[1];
+          out[2] = val[2];
+          out[3] = val[3];
         }
-        wave_sync();
       };
 
       auto next_off = [&](int r) __attribute__((always_inline)) {
         return key_offset(readlane(tb.vk, min(r, kLanes - 1)));
       };
-      fetch(next_off(0), stg);
+      fetch(next_off(0));
       int r = 0, base = 0, np = 0;
       for (;;) {
-        // run r: its coefficients go from `stg` to LDS, the next run's into `stg`
-        put(stg);
-        fetch(next_off(r + 1), stg);
-        wave_sync();
-        read_b(Bc);
+        // run r: its coefficients are in the slot once the copy has landed;
+        // after they are read, the slot takes the next run's
+        wait_copies();
+        double Bc[2][S];
+        {
+          v4i q[S];
+          lds_read_steps<S>(bread, q);
+#pragma unroll
+          for (int st = 0; st < S; ++st) {
+            const Pair<double> v = __builtin_bit_cast(Pair<double>, q[st]);
+            Bc[0][st] = v.x;
+            Bc[1][st] = v.y;
+          }
+        }
+        fetch(next_off(r + 1));
         const int Sr = readlane(tb.vs, r);
         const int Er = r + 1 < kLanes ? readlane(tb.vs, r + 1) : tb.n;
         int p[2] = {0, 0};
@@ -1107,19 +1166,17 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
               d0 = mfma4(A[b][s], Bc[0][s], d0);
               d1 = mfma4(A[b][s], Bc[1][s], d1);
             }
-            // sum the four channel quarters into the lanes of quarter 3
+            // sum the four channel blocks into the lanes of block 3
             d0 += row_shr<4>(d0);
             d1 += row_shr<4>(d1);
             d0 += row_shr<8>(d0);
             d1 += row_shr<8>(d1);
-            if (h == 3 && x < 3) {   // P[k = kk][q = 2x + c] (row k: 6 doubles)
-              *reinterpret_cast<Pair<double>*>(__builtin_assume_aligned(
-                  store + np * kPairDoubles + 6 * kk + 2 * x, 16)) = Pair<double>{d0, d1};
-            }
+            if (h == 3 && x < 3)   // P[k = kk][q = 2x + c] (row k: 6 doubles)
+              lds_write16(store + (uint32_t)((np * kPairDoubles + 6 * kk + 2 * x) * sizeof(double)),
+                          __builtin_bit_cast(v4i, Pair<double>{d0, d1}));
             ++np;
           }
         }
-        wave_sync();   // the slot is rewritten by the next run
         if (np > kPairSlots - NB) {  // the next run may add NB products
           eval(base, np);
           base += np;
@@ -1130,15 +1187,8 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
       if (np > 0) eval(base, np);
     }
     // each lane writes the dE/dR~ row of its own slot (zero for padding)
-    if (tb.rank >= -1) {
-      double v[4] = {0.0, 0.0, 0.0, 0.0};
-      if (tb.rank >= 0) {
-        const double* src = reinterpret_cast<const double*>(&zrec<double>(smem, zoff, tb.rank));
-#pragma unroll
-        for (int k = 0; k < 4; ++k) v[k] = src[k];
-      }
-      store_row(dR + ((size_t)(i0 + lane / kC) * nnei + s0 + lane % kC) * 4, v);
-    }
+    if (tb.rank >= -1)
+      store_row(dR + ((size_t)(i0 + lane / kC) * nnei + s0 + lane % kC) * 4, out);
     wave_sync();
   }
 }
@@ -1224,23 +1274,24 @@ int launch_fwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
 }
 
 // float64 with M1 <= 128: the matrix-core kernel, ceil(M1 / 16) K steps per
-// channel quarter, an interval (48 ld bytes) staged by ceil(48 ld / 1024)
-// loads, so that only the last one runs past the interval
+// channel block, an interval copied by mfma_slot_kib(S, ld) loads (ld lies in
+// [16 S - 12, 16 S], so that count takes one of two values per S)
 template <int S>
 void launch_mfma_s(hipStream_t s, const Geo& g, dim3 grid, dim3 block, const void* coeff,
                    const int* atype, const int* nlist, const void* em, const void* dT, void* dR) {
-  const int ns = (48 * g.ld + 1023) / 1024;
+  const int ns = mfma_slot_kib(S, g.ld);
   auto go = [&](auto kern, size_t wave_bytes) {
     hipLaunchKernelGGL(kern, grid, block, kWaves * wave_bytes, s, g, (const double*)coeff,
                        atype, nlist, (const double*)em, (const double*)dT, (double*)dR);
   };
-  constexpr int lo = (48 * (16 * S - 12) + 1023) / 1024;   // smallest ld of this S
+  constexpr int lo = mfma_slot_kib(S, 16 * S - 12);
+  static_assert(mfma_slot_kib(S, 16 * S) <= lo + 1, "two slot sizes per S");
   if (g.ntypes == 1) {
-    if (ns <= lo) go(se_a_bwd_mfma_kernel<S, lo, true>, bwdm_wave_bytes(lo, g.ld));
-    else go(se_a_bwd_mfma_kernel<S, lo + 1, true>, bwdm_wave_bytes(lo + 1, g.ld));
+    if (ns <= lo) go(se_a_bwd_mfma_kernel<S, lo, true>, bwdm_wave_bytes(lo));
+    else go(se_a_bwd_mfma_kernel<S, lo + 1, true>, bwdm_wave_bytes(lo + 1));
   } else {
-    if (ns <= lo) go(se_a_bwd_mfma_kernel<S, lo, false>, bwdm_wave_bytes(lo, g.ld));
-    else go(se_a_bwd_mfma_kernel<S, lo + 1, false>, bwdm_wave_bytes(lo + 1, g.ld));
+    if (ns <= lo) go(se_a_bwd_mfma_kernel<S, lo, false>, bwdm_wave_bytes(lo));
+    else go(se_a_bwd_mfma_kernel<S, lo + 1, false>, bwdm_wave_bytes(lo + 1));
   }
 }
 
