@@ -39,6 +39,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <type_traits>
 
 #include "dpc.h"
 
@@ -322,7 +323,8 @@ __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[
                                                   int s0, int wbase, uint32_t vm,
                                                   const TI* __restrict__ em, Rec<TI>* z,
                                                   ChunkScratch& W, int lane,
-                                                  int* pair = nullptr, Rec<TI>* mine = nullptr) {
+                                                  int* pair = nullptr, Rec<TI>* mine = nullptr,
+                                                  bool use_pre = false, const TI* pre = nullptr) {
   constexpr int kC = kLanes / NB;
   const int a = lane / kC, sl = lane % kC, j = s0 + sl;
   int at = -1;
@@ -340,7 +342,12 @@ __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[
     const size_t row = (size_t)(i0 + a) * g.nnei + j;
     valid = (holder >> (il >> 6)) & 1;
     if (valid) {
-      load_row(em + row * 4, rec.r);
+      if (use_pre) {    // the caller has loaded the row already
+#pragma unroll
+        for (int k = 0; k < 4; ++k) rec.r[k] = pre[k];
+      } else {
+        load_row(em + row * 4, rec.r);
+      }
       // one type (kOne): the pair range is uniform (scalar loads); else per lane
       int blk = 0;
       PairRange P;
@@ -983,18 +990,14 @@ __device__ __forceinline__ void lds_read_steps(uint32_t a, v4i (&q)[S]) {
 #undef DPC_R
 }
 
-// One product, 4 rows of 6 doubles at a (12 reads of 16 bytes).
-__device__ __forceinline__ void lds_read_pair(uint32_t a, v4i (&q)[12]) {
+// Two rows (12 doubles) of a product at a (6 reads of 16 bytes).
+__device__ __forceinline__ void lds_read_rows2(uint32_t a, v4i (&q)[6]) {
   asm volatile(
       "ds_read_b128 %0, %[a]\n\tds_read_b128 %1, %[a] offset:16\n\t"
       "ds_read_b128 %2, %[a] offset:32\n\tds_read_b128 %3, %[a] offset:48\n\t"
       "ds_read_b128 %4, %[a] offset:64\n\tds_read_b128 %5, %[a] offset:80\n\t"
-      "ds_read_b128 %6, %[a] offset:96\n\tds_read_b128 %7, %[a] offset:112\n\t"
-      "ds_read_b128 %8, %[a] offset:128\n\tds_read_b128 %9, %[a] offset:144\n\t"
-      "ds_read_b128 %10, %[a] offset:160\n\tds_read_b128 %11, %[a] offset:176\n\t"
       "s_waitcnt lgkmcnt(0)"
-      : "=&v"(q[0]), "=&v"(q[1]), "=&v"(q[2]), "=&v"(q[3]), "=&v"(q[4]), "=&v"(q[5]),
-        "=&v"(q[6]), "=&v"(q[7]), "=&v"(q[8]), "=&v"(q[9]), "=&v"(q[10]), "=&v"(q[11])
+      : "=&v"(q[0]), "=&v"(q[1]), "=&v"(q[2]), "=&v"(q[3]), "=&v"(q[4]), "=&v"(q[5])
       : [a] "v"(a)
       : "memory");
 }
@@ -1078,6 +1081,8 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
   const int nch = (nnei + kC - 1) / kC;
   int s0 = ((int)(blockIdx.x * 5 + wave * 3) % nch) * kC;
   uint32_t vm = 0, occ = 0;
+  double pre[4];      // R~ rows of chunk set pre_s0, loaded ahead (valid slots use them)
+  int pre_s0 = -1;
   for (int cc = 0, wbase = -1; cc < nch; ++cc, s0 = s0 + kC < nnei ? s0 + kC : 0) {
     if (s0 - s0 % (kWindow / NB) != wbase) {  // window of nlist signs holding s0
       wbase = s0 - s0 % (kWindow / NB);
@@ -1091,21 +1096,25 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
     int pair;
     Rec<double> mine;
     const Tables tb = build_chunk_set<double, double, NB, true, kOne, true>(
-        g, ai, i0, s0, wbase, vm, em, nullptr, W, lane, &pair, &mine);
+        g, ai, i0, s0, wbase, vm, em, nullptr, W, lane, &pair, &mine, pre_s0 == s0, pre);
+    // the rows of the next chunk set are loaded during this one's last run
+    const int s0n = s0 + kC < nnei ? s0 + kC : 0;
+    const bool more = cc + 1 < nch;
     double out[4] = {0.0, 0.0, 0.0, 0.0};   // this lane's dE/dR~ row
     if (tb.n > 0) {
       // the lanes whose records belong to pairs [base, base + np) read their products
       auto eval = [&](int base, int np) __attribute__((always_inline)) {
         if (pair >= base && pair < base + np) {
-          v4i q[12];
-          lds_read_pair(store + (uint32_t)((pair - base) * kPairDoubles * sizeof(double)), q);
+          const uint32_t pa = store + (uint32_t)((pair - base) * kPairDoubles * sizeof(double));
           const double t = mine.t;
           double val[4], der[4];
+          v4i q[6];
 #pragma unroll
           for (int k = 0; k < 4; ++k) {
-            const Pair<double> c01 = __builtin_bit_cast(Pair<double>, q[3 * k]);
-            const Pair<double> c23 = __builtin_bit_cast(Pair<double>, q[3 * k + 1]);
-            const Pair<double> c45 = __builtin_bit_cast(Pair<double>, q[3 * k + 2]);
+            if (k % 2 == 0) lds_read_rows2(pa + 48 * k, q);   // rows k and k + 1
+            const Pair<double> c01 = __builtin_bit_cast(Pair<double>, q[3 * (k % 2)]);
+            const Pair<double> c23 = __builtin_bit_cast(Pair<double>, q[3 * (k % 2) + 1]);
+            const Pair<double> c45 = __builtin_bit_cast(Pair<double>, q[3 * (k % 2) + 2]);
             double v = c45.y, d = c45.y;
             v = fma(v, t, c45.x);
             d = fma(d, t, v);
@@ -1133,10 +1142,12 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
         return key_offset(readlane(tb.vk, min(r, kLanes - 1)));
       };
       fetch(next_off(0));
-      int r = 0, base = 0, np = 0;
-      for (;;) {
-        // run r: its coefficients are in the slot once the copy has landed;
-        // after they are read, the slot takes the next run's
+      int base = 0, np = 0;
+      // run r: its coefficients are in the slot once the copy has landed;
+      // after they are read, the slot takes the next run's (kLast: the
+      // last run loads the next chunk set's rows instead)
+      auto run = [&](int r, auto last) __attribute__((always_inline)) {
+        constexpr bool kLast = decltype(last)::value;
         wait_copies();
         double Bc[2][S];
         {
@@ -1149,7 +1160,13 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
             Bc[1][st] = v.y;
           }
         }
-        fetch(next_off(r + 1));
+        if constexpr (!kLast) {
+          fetch(next_off(r + 1));
+        } else if (more) {
+          const int ia = min(i0 + lane / kC, g.nloc - 1), j = min(s0n + lane % kC, nnei - 1);
+          load_row(em + ((size_t)ia * nnei + j) * 4, pre);
+          pre_s0 = s0n;
+        }
         const int Sr = readlane(tb.vs, r);
         const int Er = r + 1 < kLanes ? readlane(tb.vs, r + 1) : tb.n;
         int p[2] = {0, 0};
@@ -1177,14 +1194,14 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
             ++np;
           }
         }
-        if (np > kPairSlots - NB) {  // the next run may add NB products
+        if (kLast || np > kPairSlots - NB) {  // the next run may add NB products
           eval(base, np);
           base += np;
           np = 0;
         }
-        if (++r == tb.nruns) break;
-      }
-      if (np > 0) eval(base, np);
+      };
+      for (int r = 0; r + 1 < tb.nruns; ++r) run(r, std::false_type{});
+      run(tb.nruns - 1, std::true_type{});
     }
     // each lane writes the dE/dR~ row of its own slot (zero for padding)
     if (tb.rank >= -1)
