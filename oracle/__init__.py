@@ -8,8 +8,9 @@ arXiv:2107.02103, Sec. II) in float64:
                (forward mode), the functions that are tabulated;
 * ``table`` -- the piecewise fifth-order Hermite table (the coefficient
                closed forms of Sec. II) and its evaluation;
-* ``se_a``  -- forward T = G^T R~ and D = T T<^T, and the backward pass
-               dE/dR~ from dE/dT, evaluated naively pair by pair;
+* ``se_a``  -- forward T = G^T R~ and D = T T<^T, the backward pass
+               dE/dR~ from dE/dT, evaluated naively pair by pair, and the
+               descriptor backward dE/dT from dE/dD;
 * ``cref``  -- the same forward/backward as plain C loops (OpenMP over atoms)
                for the large workloads.
 

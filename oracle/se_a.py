@@ -106,6 +106,30 @@ def forward_untabulated(em, nlist, atype, nets, sel, m2, atoms=None):
     return T, D
 
 
+def descriptor_backward(T, dD):
+    """dE/dT [n, M, 4] from dE/dD [n, M, M'] (Sec. II: D_i = T_i (T_i<)^T,
+    T_i< the first M' rows of T_i).  D[m][n] = sum_k T[m][k] T[n][k] holds
+    T twice, once through row m and once through row n < M', so
+
+        dE/dT[m][k] = sum_{n<M'} dE/dD[m][n] T[n][k]
+                      + (m < M') sum_{m'} dE/dD[m'][m] T[m'][k].
+
+    Written as two explicit loops over the atom's entries."""
+    n_at, M, m2 = dD.shape
+    dT = np.zeros((n_at, M, 4))
+    for a in range(n_at):
+        for m in range(M):
+            for k in range(4):
+                v = 0.0
+                for n in range(m2):
+                    v += dD[a, m, n] * T[a, n, k]
+                if m < m2:
+                    for q in range(M):
+                        v += dD[a, q, m] * T[a, q, k]
+                dT[a, m, k] = v
+    return dT
+
+
 def energy(T, lam):
     """Scalar E = sum <Lambda_i, T_i> whose dE/dT is Lambda (FD pins)."""
     return float(np.sum(T * lam))

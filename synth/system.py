@@ -216,12 +216,14 @@ def _chunk(cfg, basis, types, disp, sel, sel_off, cand, b, c0, c1, nlist, em):
     return stats, smax, int(ok.sum())
 
 
-def random_grad(rng, nat, m1, threads=None, chunk=65536):
-    """dE/dT ~ N(0, 1) of shape [nat, m1, 4], drawn in fixed chunks of atoms
-    from streams spawned off ``rng`` (deterministic for any thread count)."""
+def random_grad(rng, nat, m1, threads=None, chunk=65536, width=4):
+    """dE/dT ~ N(0, 1) of shape [nat, m1, width] (width 4: dE/dT; width M':
+    dE/dD, or a T-shaped input of the descriptor backward), drawn in fixed
+    chunks of atoms from streams spawned off ``rng`` (deterministic for any
+    thread count)."""
     from concurrent.futures import ThreadPoolExecutor
     import os
-    out = np.empty((nat, m1, 4))
+    out = np.empty((nat, m1, width))
     starts = list(range(0, nat, chunk))
     seeds = rng.bit_generator.seed_seq.spawn(len(starts))
     threads = threads or max(1, min(16, len(os.sched_getaffinity(0))))
@@ -229,7 +231,7 @@ def random_grad(rng, nat, m1, threads=None, chunk=65536):
     def run(k):
         a0 = starts[k]
         a1 = min(nat, a0 + chunk)
-        out[a0:a1] = np.random.default_rng(seeds[k]).standard_normal((a1 - a0, m1, 4))
+        out[a0:a1] = np.random.default_rng(seeds[k]).standard_normal((a1 - a0, m1, width))
 
     with ThreadPoolExecutor(threads) as ex:
         list(ex.map(run, range(len(starts))))
