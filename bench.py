@@ -31,8 +31,9 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash():
-    p = os.path.join(ROOT, "paper_2107_02103_amd", "csrc", "dpc_se_a.hip")
+def kernel_source_hash(kernel="se_a"):
+    src = "dpc_descriptor.hip" if kernel.startswith("descriptor") else "dpc_se_a.hip"
+    p = os.path.join(ROOT, "paper_2107_02103_amd", "csrc", src)
     return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
 
 
@@ -43,7 +44,7 @@ def hbm_traffic(cfg_name, kernel):
     if not os.path.exists(p):
         return None
     d = json.load(open(p))
-    if d.get("kernel_source_sha256_16") != kernel_source_hash():
+    if d.get("kernel_source_sha256_16") != kernel_source_hash(kernel):
         return None
     return d.get("hbm_bytes_per_launch")
 
@@ -92,6 +93,71 @@ def copy_probe(mib):
     print(json.dumps({"copy_probe_bytes": n * 8, "launches": 3}), flush=True)
 
 
+def bench_descriptor_bwd(args):
+    """dpc_descriptor_bwd (dE/dT from dE/dD and T) over the configuration's
+    atoms with M = 100, M' = 16: seeded standard-normal T and dE/dD resident
+    in HBM, HIP events around each launch on the launch stream.  The kernel
+    is bound by HBM bandwidth: 8 (4 M + M M' + 4 M) bytes per atom in float64."""
+    import numpy as np
+    import torch
+    import paper_2107_02103_amd as P
+    from synth.configs import get_config
+    from synth.system import random_grad
+    from oracle.se_a import descriptor_backward
+
+    key = int(args.config) if args.config.isdigit() else args.config
+    cfg = get_config(key)
+    n, m1, m2 = cfg.natoms, cfg.m1, cfg.m2
+    log(f"[bench] descriptor backward: generating T and dE/dD for {n} atoms")
+    rng = np.random.default_rng([2107_02103, 77, 3])
+    T = random_grad(rng, n, m1)
+    dD = random_grad(rng, n, m1, width=m2)
+    Tg, Dg = torch.from_numpy(T).cuda(), torch.from_numpy(dD).cuda()
+    out = torch.empty_like(Tg)
+    s = torch.cuda.Stream()
+    run = lambda: P.dpc_descriptor_bwd(s, P.DPC_F64, n, m1, m2, Tg, Dg, out)
+    with torch.cuda.stream(s):
+        for _ in range(args.warmup):
+            run()
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        t0 = time.perf_counter()
+        for e0, e1 in evs:
+            e0.record(s)
+            run()
+            e1.record(s)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+    ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    nbytes = 8.0 * (4 * m1 + m1 * m2 + 4 * m1) * n
+    achieved = nbytes / (ms * 1e-3) / 1e9
+    res = {
+        "metric": "descriptor backward dE/dT from dE/dD (fp64), atoms/s + % of HBM bandwidth",
+        "value": n * args.steps / wall, "unit": "atoms/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": wall / args.steps * 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": f"{cfg.name} descriptor: {n} atoms, M {m1}, M2 {m2}, "
+                               "T and dE/dD standard normal", "atoms": n},
+        "kernel_ms": ms,
+        "roofline": {"bound": "hbm", "kernel": "descriptor_bwd_kernel", "achieved": achieved,
+                     "peak": 8000.0, "unit": "GB/s", "frac": achieved / 8000.0,
+                     "traffic": hbm_traffic(cfg.name, "descriptor_bwd_kernel")},
+    }
+    del Tg, Dg, out
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        # the oracle (plain Python loops, one core) on the first atoms for ~cpu_seconds
+        t0, done = time.perf_counter(), 0
+        while done < n and time.perf_counter() - t0 < args.cpu_seconds:
+            descriptor_backward(T[done:done + 16], dD[done:done + 16])
+            done += 16
+        dt = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": done / dt, "unit": "atoms/s", "cores": 1, "kind": "oracle",
+                               "sample": f"atoms 0..{done - 1} of {n}, {dt:.1f} s"}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -101,6 +167,8 @@ def main():
     ap.add_argument("--dtype", default=None, choices=[None, "f64", "f32", "f32acc64"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--descriptor-bwd", action="store_true",
+                    help="time the descriptor backward (dE/dT from dE/dD) instead of the se_a step")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (3 times), the known-size "
                          "kernel that calibrates the HBM byte counters, and exit")
@@ -113,6 +181,9 @@ def main():
 
     if args.copy_probe_mib:
         copy_probe(args.copy_probe_mib)
+        return
+    if args.descriptor_bwd:
+        bench_descriptor_bwd(args)
         return
 
     import numpy as np

@@ -151,6 +151,23 @@ int dpc_se_a_tab_bwd(void* stream, dpc_dtype dtype, int nloc, int ntypes, const 
                      const int* atype, const int* nlist, const void* em,
                      const void* dE_dT, void* dE_dem);
 
+/* Backward of the descriptor (paper Sec. II: D_i = T_i (T_i<)^T, T_i< the
+ * first m2 rows of T_i, i.e. D_i[m][n] = sum_k T_i[m][k] T_i[n][k], n < m2):
+ *   dE/dT_i[m][k] = sum_{n<m2} dE/dD_i[m][n] T_i[n][k]
+ *                 + (m < m2) sum_{m'} dE/dD_i[m'][m] T_i[m'][k].
+ * Its output is the dE_dT input of dpc_se_a_tab_bwd, so that a caller holding
+ * dE/dD (from the fitting net) and the forward's T gets dE/dR~ in two calls.
+ *   T        device [nloc][m1][4], the forward's T (float64, or float32 for DPC_F32)
+ *   dE_dD    device [nloc][m1][m2], same type as T
+ *   dE_dT    device out [nloc][m1][4]: float64 for DPC_F64, float32 otherwise
+ *            (the type dpc_se_a_tab_bwd takes); must not overlap the inputs
+ * Arithmetic is float64 except for DPC_F32.  Requires 1 <= m2 <= m1 <=
+ * DPC_MAX_M1 and (4 m1 + m1 (m2 + 1)) elements of the arithmetic type within
+ * 64 KiB (DPC_ENOTSUP otherwise; m2 = 16 allows every m1).  nloc = 0 is a
+ * no-op.  Errors and ownership as the calls above.                          */
+int dpc_descriptor_bwd(void* stream, dpc_dtype dtype, int nloc, int m1, int m2,
+                       const void* T, const void* dE_dD, void* dE_dT);
+
 #ifdef __cplusplus
 }
 #endif

@@ -32,7 +32,7 @@ DPC_OK, DPC_EINVAL, DPC_ERANGE, DPC_EHIP, DPC_ENOTSUP = 0, -1, -2, -3, -4
 DPC_F64, DPC_F32, DPC_F32_ACC64 = 0, 1, 2
 DPC_MAX_TYPES, DPC_MAX_M1 = 8, 256
 EXPORTED = ("dpc_strerror", "dpc_last_hip_error", "dpc_version", "dpc_table_layout", "dpc_build_table",
-            "dpc_se_a_tab_fwd", "dpc_se_a_tab_bwd")
+            "dpc_se_a_tab_fwd", "dpc_se_a_tab_bwd", "dpc_descriptor_bwd")
 
 
 class dpc_range(C.Structure):
@@ -62,6 +62,9 @@ _lib.dpc_se_a_tab_bwd.restype = C.c_int
 _lib.dpc_se_a_tab_bwd.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.POINTER(C.c_int),
                                   C.c_int, C.POINTER(dpc_range), C.c_void_p, C.c_void_p,
                                   C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+_lib.dpc_descriptor_bwd.restype = C.c_int
+_lib.dpc_descriptor_bwd.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p,
+                                    C.c_void_p, C.c_void_p]
 
 
 class DpcError(RuntimeError):
@@ -202,3 +205,10 @@ def dpc_se_a_tab_bwd(stream, dtype, nloc, ntypes, sel, m1, ranges, coeff, atype,
                                  _ptr(em, name="em"), _ptr(dE_dT, name="dE_dT"),
                                  _ptr(dE_dem, name="dE_dem")),
            "dpc_se_a_tab_bwd")
+
+
+def dpc_descriptor_bwd(stream, dtype, nloc, m1, m2, T, dE_dD, dE_dT):
+    _check(_lib.dpc_descriptor_bwd(_stream(stream), int(dtype), int(nloc), int(m1), int(m2),
+                                   _ptr(T, name="T"), _ptr(dE_dD, name="dE_dD"),
+                                   _ptr(dE_dT, name="dE_dT")),
+           "dpc_descriptor_bwd")

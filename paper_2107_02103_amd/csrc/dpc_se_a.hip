@@ -42,6 +42,7 @@
 #include <type_traits>
 
 #include "dpc.h"
+#include "dpc_internal.h"
 
 #ifndef DPC_FWD_ATOMS_PER_WAVE
 #define DPC_FWD_ATOMS_PER_WAVE 4
@@ -1359,6 +1360,8 @@ int launch_bwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
 }
 
 }  // namespace
+
+int dpc_internal_launch_status() { return launch_status(); }
 
 extern "C" const char* dpc_last_hip_error(void) { return hipGetErrorString(g_last_hip); }
 

@@ -57,6 +57,19 @@ class SeATab:
                            self.sel, self.m1, self.ranges, self.coeff, atype, nlist, em, dT, dR)
         return dR
 
+    def descriptor_backward(self, T, dD, dT=None, stream=None):
+        """dE/dT from dE/dD and the forward's T (the input dtype of backward())."""
+        nloc = T.shape[0]
+        if T.dtype != self.t_acc or tuple(T.shape) != (nloc, self.m1, 4):
+            raise ValueError("T has the wrong dtype or shape")
+        if dD.dtype != self.t_acc or tuple(dD.shape) != (nloc, self.m1, self.m2):
+            raise ValueError("dE/dD has the wrong dtype or shape")
+        if dT is None:
+            dT = torch.empty((nloc, self.m1, 4), dtype=self.t_in, device=self.device)
+        B.dpc_descriptor_bwd(stream or torch.cuda.current_stream(), self.dtype, nloc, self.m1,
+                             self.m2, T, dD, dT)
+        return dT
+
     def _check(self, em, nlist, atype):
         nloc = nlist.shape[0]
         if em.dtype != self.t_in or tuple(em.shape) != (nloc, self.nnei, 4):

@@ -162,3 +162,20 @@ def test_kernel_entry_points_validate_before_launch():
     # nloc = 0 is a no-op that launches nothing
     P.dpc_se_a_tab_fwd(0, P.DPC_F64, 0, 2, sel, 8, 4, r, 0, 0, 0, 0, 0, 0)
     P.dpc_se_a_tab_bwd(0, P.DPC_F64, 0, 2, sel, 8, r, 0, 0, 0, 0, 0, 0)
+
+
+def test_descriptor_bwd_validates_before_launch():
+    fake = 4096  # never dereferenced: validation fails first
+    cases = [((9, 3, 8, 4), B.DPC_EINVAL), ((0, -1, 8, 4), B.DPC_EINVAL), ((0, 3, 8, 9), B.DPC_EINVAL),
+             ((0, 3, 8, 0), B.DPC_EINVAL), ((0, 3, 0, 1), B.DPC_EINVAL), ((0, 3, 300, 4), B.DPC_ENOTSUP)]
+    for (dt, nloc, m1, m2), code in cases:
+        with pytest.raises(P.DpcError) as e:
+            P.dpc_descriptor_bwd(0, dt, nloc, m1, m2, fake, fake, fake)
+        assert e.value.status == code, (dt, nloc, m1, m2)
+    for i in range(3):                                                # a null buffer
+        ptrs = [fake, fake, fake]
+        ptrs[i] = 0
+        with pytest.raises(P.DpcError) as e:
+            P.dpc_descriptor_bwd(0, P.DPC_F64, 3, 8, 4, *ptrs)
+        assert e.value.status == B.DPC_EINVAL
+    P.dpc_descriptor_bwd(0, P.DPC_F64, 0, 8, 4, 0, 0, 0)              # nloc = 0: no-op
