@@ -140,9 +140,9 @@ def bench_descriptor_bwd(args):
         "config": {"workload": f"{cfg.name} descriptor: {n} atoms, M {m1}, M2 {m2}, "
                                "T and dE/dD standard normal", "atoms": n},
         "kernel_ms": ms,
-        "roofline": {"bound": "hbm", "kernel": "descriptor_bwd_kernel", "achieved": achieved,
+        "roofline": {"bound": "hbm", "kernel": "descriptor_bwd_m16_kernel", "achieved": achieved,
                      "peak": 8000.0, "unit": "GB/s", "frac": achieved / 8000.0,
-                     "traffic": hbm_traffic(cfg.name, "descriptor_bwd_kernel")},
+                     "traffic": hbm_traffic(cfg.name, "descriptor_bwd_m16_kernel")},
     }
     del Tg, Dg, out
     torch.cuda.empty_cache()
