@@ -167,6 +167,9 @@ def main():
     ap.add_argument("--dtype", default=None, choices=[None, "f64", "f32", "f32acc64"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--stride", type=float, default=None,
+                    help="table stride d1 on the observed range (band stride 10 x d1; default: the "
+                         "workload's 0.01 / 0.1), for the stride study")
     ap.add_argument("--descriptor-bwd", action="store_true",
                     help="time the descriptor backward (dE/dT from dE/dD) instead of the se_a step")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -194,6 +197,8 @@ def main():
 
     key = int(args.config) if args.config.isdigit() else args.config
     cfg = get_config(key)
+    if args.stride:
+        cfg = cfg.with_(d1=args.stride, d2=10 * args.stride)
     dtype = args.dtype or cfg.dtype
     mode = {"f64": P.DPC_F64, "f32": P.DPC_F32, "f32acc64": P.DPC_F32_ACC64}[dtype]
     store = np.float64 if dtype == "f64" else np.float32
@@ -268,14 +273,15 @@ def main():
                                f"rc {cfg.rc}, rcs {cfg.rcs}, sel {list(cfg.sel)}, "
                                f"embedding {'-'.join(map(str, cfg.widths))}, M2 {cfg.m2}, "
                                f"table stride {cfg.d1}/{cfg.d2}",
-                   "atoms": atoms, "valid_pairs": pairs, "nnei": cfg.nnei},
+                   "atoms": atoms, "valid_pairs": pairs, "nnei": cfg.nnei,
+                   "table_bytes": int(op.coeff.numel() * op.coeff.element_size())},
         "tflops_algorithmic": tflops,
         "frac_vector_peak": tflops / peak,
         "fwd_ms": fwd_ms,
         "bwd_ms": bwd_ms,
         "roofline": {"bound": bound, "kernel": dom, "achieved": achieved, "peak": peak,
                      "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": hbm_traffic(cfg.name, dom)},
+                     "traffic": None if args.stride else hbm_traffic(cfg.name, dom)},
     }
     del T, D, dR, em, dT
     torch.cuda.empty_cache()

@@ -22,7 +22,7 @@ rows of one sel block at a time and a matmul for the contraction.
 """
 import numpy as np
 
-from .net import embed
+from .net import embed, embed_d2
 
 
 def _blocks(sel):
@@ -104,6 +104,27 @@ def forward_untabulated(em, nlist, atype, nets, sel, m2, atoms=None):
             T[n] += G.T @ R
     D = T @ np.transpose(T[:, :m2, :], (0, 2, 1))
     return T, D
+
+
+def backward_untabulated(em, nlist, atype, nets, sel, dT, atoms=None):
+    """dE/dR~ through the original (uncompressed) embedding net: the backward
+    formula of this module with g, g' replaced by G and G' of the net (its
+    forward-mode first derivative) -- the reference of the table-stride
+    study on small inputs."""
+    nt = len(sel)
+    atoms = np.arange(nlist.shape[0]) if atoms is None else np.asarray(atoms)
+    dR = np.zeros((len(atoms),) + em.shape[1:])
+    for n, i in enumerate(atoms):
+        dTi = dT[i]
+        for beta, s0, s1 in _blocks(sel):
+            js = s0 + np.nonzero(nlist[i, s0:s1] >= 0)[0]
+            if len(js) == 0:
+                continue
+            R = em[i, js]
+            G, Gp, _ = embed_d2(R[:, 0], nets[atype[i] * nt + beta])
+            dR[n, js] = G @ dTi
+            dR[n, js, 0] += np.sum(Gp * (R @ dTi.T), axis=1)
+    return dR
 
 
 def descriptor_backward(T, dD):

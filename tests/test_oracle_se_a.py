@@ -3,7 +3,7 @@ import numpy as np
 import pytest
 
 from oracle import cref
-from oracle.se_a import backward, energy, forward, forward_untabulated
+from oracle.se_a import backward, backward_untabulated, energy, forward, forward_untabulated
 from oracle.table import build_tables
 
 
@@ -140,3 +140,28 @@ def test_c_oracle_matches_numpy_oracle(tiny_inputs, key):
     # chunked ranges give the same rows
     T2, _ = pb.forward(7, 19)
     np.testing.assert_array_equal(T2, T[7:19])
+
+
+def test_backward_untabulated_central_difference(tiny_inputs):
+    # E = <Lambda, T(R~)> through the real net: against central differences of
+    # forward_untabulated, and close to the tabulated backward
+    x, tabs = _case(tiny_inputs, "tiny_water")
+    atoms = np.arange(0, len(x.nlist), max(1, len(x.nlist) // 4))[:4]
+    rng = np.random.default_rng(12)
+    lam = rng.normal(size=(len(x.nlist), x.cfg.m1, 4))
+    dR = backward_untabulated(x.em, x.nlist, x.atype, x.nets, x.cfg.sel, lam, atoms=atoms)
+    dRt = backward(x.em, x.nlist, x.atype, tabs, x.cfg.sel, lam, atoms=atoms)
+    assert np.max(np.abs(dR - dRt)) <= 1e-8 * np.max(np.abs(dR))
+    h = 1e-6
+    worst = 0.0
+    for n, i in enumerate(atoms):
+        js = np.nonzero(x.nlist[i] >= 0)[0]
+        for j in js[rng.choice(len(js), size=min(4, len(js)), replace=False)]:
+            for k in range(4):
+                ep = x.em[i:i + 1].copy(); em_ = x.em[i:i + 1].copy()
+                ep[0, j, k] += h; em_[0, j, k] -= h
+                Tp, _ = forward_untabulated(ep, x.nlist[i:i + 1], x.atype[i:i + 1], x.nets, x.cfg.sel, x.cfg.m2)
+                Tm, _ = forward_untabulated(em_, x.nlist[i:i + 1], x.atype[i:i + 1], x.nets, x.cfg.sel, x.cfg.m2)
+                fd = (energy(Tp, lam[i:i + 1]) - energy(Tm, lam[i:i + 1])) / (2 * h)
+                worst = max(worst, abs(fd - dR[n, j, k]) / np.max(np.abs(dR[n, j])))
+    assert worst <= 1e-6, worst
