@@ -43,6 +43,7 @@ class Inputs:
     stats: Dict                  # per centre type: mean, sigma, sigma_all
     dT: np.ndarray = None        # float64 [nloc, m1, 4] upstream gradient dE/dT
     n_valid: int = 0
+    coords: np.ndarray = None    # float64 [nloc, 3] positions (cubic periodic box of edge cfg.box)
 
     @property
     def d1(self) -> float:
@@ -330,6 +331,10 @@ def make_inputs(cfg: Config, chunk_cells: int = 2048, with_grad: bool = True,
     nets = [random_net(rng_nets, cfg.widths) for _ in range(npair)]
     dT = random_grad(rng_grad, nat, cfg.m1, threads) if with_grad else None
     st = {"mean": mean, "sigma": sig, "sigma_all": sig_all, "dmax": dmax}
+    # positions: cell c = i // nb at (c // N^2, (c // N) % N, c % N) * L, plus the basis site and displacement
+    c = np.arange(nat) // nb
+    cell = np.stack([c // (N * N), (c // N) % N, c % N], 1).astype(np.float64)
+    coords = cell * L + basis[np.arange(nat) % nb] + disp
     return Inputs(cfg=cfg, atype=types.astype(np.int32), nlist=nlist, em=em, nets=nets,
                   lo=lo, L1=L1, L2=L2, s_hat_max=shmax, stats=st, dT=dT,
-                  n_valid=n_valid)
+                  n_valid=n_valid, coords=coords)
