@@ -168,6 +168,57 @@ int dpc_se_a_tab_bwd(void* stream, dpc_dtype dtype, int nloc, int ntypes, const 
 int dpc_descriptor_bwd(void* stream, dpc_dtype dtype, int nloc, int m1, int m2,
                        const void* T, const void* dE_dD, void* dE_dT);
 
+/* Environment matrix R~ from positions (paper Sec. II, Eq. (1) and the
+ * normalisation after it).  For slot s of atom i with j = nlist[i][s] >= 0:
+ * r_ij = r_j - r_i as the minimum image in a cubic periodic box of edge `box`,
+ * r = |r_ij|, s(r) = 1/r (r < rcs), (1/r)[u^3(-6u^2+15u-10)+1] (rcs <= r < rc,
+ * u = (r - rcs)/(rc - rcs)), 0 (r >= rc), and the row is
+ *   ((s - mean[t]) / sigma[t], s x / sigma_all[t], s y / sigma_all[t], s z / sigma_all[t]),
+ * t = atype[i]; padding rows (nlist < 0) are zero.
+ *   box, rc, rcs  require 0 <= rcs < rc and box > 2 rc (else DPC_ERANGE)
+ *   mean, sigma, sigma_all  host [ntypes], sigma and sigma_all > 0
+ *   coord    device float64 [nloc][3]
+ *   atype    device int32 [nloc]; nlist device int32 [nloc][nnei], entries < nloc
+ *            (a row with an out-of-range type or neighbour index becomes NaN)
+ *   em       device out [nloc][nnei][4]: float64 for DPC_F64, float32 otherwise
+ *            (the em input of dpc_se_a_tab_fwd / _bwd in that mode)
+ * Arithmetic is float64.  nloc = 0 is a no-op.                              */
+int dpc_env_mat_a(void* stream, dpc_dtype dtype, int nloc, int ntypes, int nnei, double box,
+                  double rc, double rcs, const double* mean, const double* sigma,
+                  const double* sigma_all, const double* coord, const int* atype,
+                  const int* nlist, void* em);
+
+/* Reverse slots of a neighbour list, for dpc_force_a: rev[i][s] = the slot of
+ * i in the list of j = nlist[i][s], searched in the sel block of i's type
+ * (sel as in dpc_se_a_tab_fwd), or -1 if i is not there (and for padding).
+ * Lists sorted by distance within each block are searched by bisection;
+ * other orders are scanned, with the same result.  Build it once per
+ * neighbour list.
+ *   coord device float64 [nloc][3], cubic box of edge `box` (minimum image)
+ *   rev   device out int32 [nloc][nnei]                                      */
+int dpc_nlist_reverse(void* stream, int nloc, int ntypes, const int* sel, double box,
+                      const double* coord, const int* atype, const int* nlist, int* rev);
+
+/* Forces and per-atom virials from dE/dR~ (F = -dE/dr; paper Sec. II: the
+ * forces need the derivatives of E with respect to R~).  With
+ * g_is = dE/dr_ij = sum_c dE/dR~_is[c] dR~_is[c]/dr_ij (dR~/dr from the
+ * positions, as in dpc_env_mat_a):
+ *   force[i]  = sum_s g_is - sum_s g_{j, rev[i][s]}   (j = nlist[i][s])
+ *   virial[i] = -sum_s r_is (x) g_is   (row-major 3x3: [a][b] = -sum r_a g_b)
+ * so that a neighbour list in which every pair within rc appears in both
+ * atoms' lists (no sel truncation) gives F = -dE/dr for every atom, and the
+ * summed virial is -dE/d(eps) of the homogeneous strain r_ij -> (1+eps) r_ij
+ * (transposed).  Each atom gathers its terms in a fixed order: the result is
+ * bitwise reproducible.
+ *   dE_dem  device [nloc][nnei][4]: float32 for DPC_F32, float64 otherwise
+ *   rev     from dpc_nlist_reverse for this nlist
+ *   force   device out float64 [nloc][3]; virial device out float64 [nloc][9] or NULL
+ * Other arguments as dpc_env_mat_a.  Arithmetic is float64.                 */
+int dpc_force_a(void* stream, dpc_dtype dtype, int nloc, int ntypes, int nnei, double box,
+                double rc, double rcs, const double* sigma, const double* sigma_all,
+                const double* coord, const int* atype, const int* nlist, const int* rev,
+                const void* dE_dem, double* force, double* virial);
+
 #ifdef __cplusplus
 }
 #endif

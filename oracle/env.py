@@ -43,19 +43,22 @@ def weight(r, rc, rcs):
     return s, ds
 
 
-def pair_vectors(coords, box, nlist):
+def pair_vectors(coords, box, nlist, atoms=None):
     """r_ij = r_j - r_i, minimum image in a cubic box of edge ``box``; zero
-    for padding slots.  [n, nnei, 3]"""
+    for padding slots.  [n, nnei, 3]; row n of ``nlist`` belongs to atom
+    ``atoms[n]`` (default: atom n)."""
     n, nnei = nlist.shape
+    atoms = np.arange(n) if atoms is None else np.asarray(atoms)
     rij = np.zeros((n, nnei, 3))
-    for i in range(n):
+    for row in range(n):
+        i = atoms[row]
         for s in range(nnei):
-            j = nlist[i, s]
+            j = nlist[row, s]
             if j < 0:
                 continue
             d = coords[j] - coords[i]
             d = d - box * np.round(d / box)
-            rij[i, s] = d
+            rij[row, s] = d
     return rij
 
 
@@ -71,9 +74,10 @@ def rows_from_vectors(rij, valid, atype, rc, rcs, mean, sigma, sigma_all):
     return em
 
 
-def env_mat(coords, box, atype, nlist, rc, rcs, mean, sigma, sigma_all):
-    """R~ [n, nnei, 4] of atoms 0..n-1."""
-    rij = pair_vectors(coords, box, nlist)
+def env_mat(coords, box, atype, nlist, rc, rcs, mean, sigma, sigma_all, atoms=None):
+    """R~ [n, nnei, 4] of atoms 0..n-1, or of ``atoms`` (then ``atype`` and
+    ``nlist`` are those atoms' rows)."""
+    rij = pair_vectors(coords, box, nlist, atoms)
     return rows_from_vectors(rij, nlist >= 0, atype, rc, rcs, mean, sigma, sigma_all)
 
 

@@ -32,7 +32,8 @@ DPC_OK, DPC_EINVAL, DPC_ERANGE, DPC_EHIP, DPC_ENOTSUP = 0, -1, -2, -3, -4
 DPC_F64, DPC_F32, DPC_F32_ACC64 = 0, 1, 2
 DPC_MAX_TYPES, DPC_MAX_M1 = 8, 256
 EXPORTED = ("dpc_strerror", "dpc_last_hip_error", "dpc_version", "dpc_table_layout", "dpc_build_table",
-            "dpc_se_a_tab_fwd", "dpc_se_a_tab_bwd", "dpc_descriptor_bwd")
+            "dpc_se_a_tab_fwd", "dpc_se_a_tab_bwd", "dpc_descriptor_bwd", "dpc_env_mat_a",
+            "dpc_nlist_reverse", "dpc_force_a")
 
 
 class dpc_range(C.Structure):
@@ -62,6 +63,18 @@ _lib.dpc_se_a_tab_bwd.restype = C.c_int
 _lib.dpc_se_a_tab_bwd.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.POINTER(C.c_int),
                                   C.c_int, C.POINTER(dpc_range), C.c_void_p, C.c_void_p,
                                   C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+_D = C.c_double
+_lib.dpc_env_mat_a.restype = C.c_int
+_lib.dpc_env_mat_a.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_int, _D, _D, _D,
+                               C.POINTER(_D), C.POINTER(_D), C.POINTER(_D), C.c_void_p, C.c_void_p,
+                               C.c_void_p, C.c_void_p]
+_lib.dpc_nlist_reverse.restype = C.c_int
+_lib.dpc_nlist_reverse.argtypes = [C.c_void_p, C.c_int, C.c_int, C.POINTER(C.c_int), _D, C.c_void_p,
+                                   C.c_void_p, C.c_void_p, C.c_void_p]
+_lib.dpc_force_a.restype = C.c_int
+_lib.dpc_force_a.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_int, _D, _D, _D,
+                             C.POINTER(_D), C.POINTER(_D), C.c_void_p, C.c_void_p, C.c_void_p,
+                             C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
 _lib.dpc_descriptor_bwd.restype = C.c_int
 _lib.dpc_descriptor_bwd.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p,
                                     C.c_void_p, C.c_void_p]
@@ -212,3 +225,40 @@ def dpc_descriptor_bwd(stream, dtype, nloc, m1, m2, T, dE_dD, dE_dT):
                                    _ptr(T, name="T"), _ptr(dE_dD, name="dE_dD"),
                                    _ptr(dE_dT, name="dE_dT")),
            "dpc_descriptor_bwd")
+
+
+def _dvec(v, n, name):
+    a = np.ascontiguousarray(v, dtype=np.float64).ravel()
+    if a.size < n:
+        raise ValueError(f"{name} needs {n} values")
+    return a.ctypes.data_as(C.POINTER(C.c_double)), a
+
+
+def dpc_env_mat_a(stream, dtype, nloc, ntypes, nnei, box, rc, rcs, mean, sigma, sigma_all, coord,
+                  atype, nlist, em):
+    pm, km = _dvec(mean, ntypes, "mean")
+    ps, ks = _dvec(sigma, ntypes, "sigma")
+    pa, ka = _dvec(sigma_all, ntypes, "sigma_all")
+    _check(_lib.dpc_env_mat_a(_stream(stream), int(dtype), int(nloc), int(ntypes), int(nnei),
+                              float(box), float(rc), float(rcs), pm, ps, pa, _ptr(coord, name="coord"),
+                              _ptr(atype, name="atype"), _ptr(nlist, name="nlist"), _ptr(em, name="em")),
+           "dpc_env_mat_a")
+
+
+def dpc_nlist_reverse(stream, nloc, ntypes, sel, box, coord, atype, nlist, rev):
+    _check(_lib.dpc_nlist_reverse(_stream(stream), int(nloc), int(ntypes), _sel(sel), float(box),
+                                  _ptr(coord, name="coord"), _ptr(atype, name="atype"),
+                                  _ptr(nlist, name="nlist"), _ptr(rev, name="rev")),
+           "dpc_nlist_reverse")
+
+
+def dpc_force_a(stream, dtype, nloc, ntypes, nnei, box, rc, rcs, sigma, sigma_all, coord, atype,
+                nlist, rev, dE_dem, force, virial=None):
+    ps, ks = _dvec(sigma, ntypes, "sigma")
+    pa, ka = _dvec(sigma_all, ntypes, "sigma_all")
+    _check(_lib.dpc_force_a(_stream(stream), int(dtype), int(nloc), int(ntypes), int(nnei),
+                            float(box), float(rc), float(rcs), ps, pa, _ptr(coord, name="coord"),
+                            _ptr(atype, name="atype"), _ptr(nlist, name="nlist"),
+                            _ptr(rev, name="rev"), _ptr(dE_dem, name="dE_dem"),
+                            _ptr(force, name="force"), _ptr(virial, name="virial")),
+           "dpc_force_a")

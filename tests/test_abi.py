@@ -179,3 +179,41 @@ def test_descriptor_bwd_validates_before_launch():
             P.dpc_descriptor_bwd(0, P.DPC_F64, 3, 8, 4, *ptrs)
         assert e.value.status == B.DPC_EINVAL
     P.dpc_descriptor_bwd(0, P.DPC_F64, 0, 8, 4, 0, 0, 0)              # nloc = 0: no-op
+
+
+def test_env_entry_points_validate_before_launch():
+    fake = 4096  # never dereferenced: validation fails first
+    m = [0.1, 0.2]; sg = [1.0, 1.0]; sa = [1.0, 1.0]
+    env = dict(stream=0, dtype=P.DPC_F64, nloc=3, ntypes=2, nnei=8, box=20.0, rc=6.0, rcs=0.5,
+               mean=m, sigma=sg, sigma_all=sa, coord=fake, atype=fake, nlist=fake, em=fake)
+    cases = [(dict(dtype=7), B.DPC_EINVAL), (dict(nloc=-1), B.DPC_EINVAL), (dict(nnei=0), B.DPC_EINVAL),
+             (dict(box=11.0), B.DPC_ERANGE), (dict(rcs=6.0), B.DPC_ERANGE), (dict(rc=-1.0), B.DPC_ERANGE),
+             (dict(sigma=[1.0, 0.0]), B.DPC_ERANGE), (dict(sigma_all=[-1.0, 1.0]), B.DPC_ERANGE),
+             (dict(ntypes=9, mean=[0.0] * 9, sigma=[1.0] * 9, sigma_all=[1.0] * 9), B.DPC_ENOTSUP),
+             (dict(coord=0), B.DPC_EINVAL), (dict(em=0), B.DPC_EINVAL)]
+    for kw, code in cases:
+        a = dict(env); a.update(kw)
+        with pytest.raises(P.DpcError) as e:
+            P.dpc_env_mat_a(**a)
+        assert e.value.status == code, kw
+    f = dict(stream=0, dtype=P.DPC_F64, nloc=3, ntypes=2, nnei=8, box=20.0, rc=6.0, rcs=0.5,
+             sigma=sg, sigma_all=sa, coord=fake, atype=fake, nlist=fake, rev=fake, dE_dem=fake,
+             force=fake, virial=None)
+    for kw, code in [(dict(box=5.0), B.DPC_ERANGE), (dict(rev=0), B.DPC_EINVAL), (dict(force=0), B.DPC_EINVAL),
+                     (dict(dtype=5), B.DPC_EINVAL)]:
+        a = dict(f); a.update(kw)
+        with pytest.raises(P.DpcError) as e:
+            P.dpc_force_a(**a)
+        assert e.value.status == code, kw
+    for kw, code in [(dict(sel=[4, -1]), B.DPC_EINVAL), (dict(box=-1.0), B.DPC_ERANGE),
+                     (dict(rev=0), B.DPC_EINVAL)]:
+        a = dict(stream=0, nloc=3, ntypes=2, sel=[4, 4], box=20.0, coord=fake, atype=fake, nlist=fake,
+                 rev=fake)
+        a.update(kw)
+        with pytest.raises(P.DpcError) as e:
+            P.dpc_nlist_reverse(**a)
+        assert e.value.status == code, kw
+    # nloc = 0: no-ops
+    P.dpc_env_mat_a(**{**env, "nloc": 0, "coord": 0, "em": 0})
+    P.dpc_force_a(**{**f, "nloc": 0, "rev": 0, "force": 0})
+    P.dpc_nlist_reverse(0, 0, 2, [4, 4], 20.0, 0, 0, 0, 0)

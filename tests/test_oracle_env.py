@@ -113,3 +113,13 @@ def test_virial_central_difference_of_strain(tiny_inputs):
             e = np.zeros((3, 3)); e[b, a] = h
             fd = (energy(e) - energy(-e)) / (2 * h)
             assert abs(-fd - W[a, b]) <= 1e-6 * np.max(np.abs(W))
+
+
+def test_env_mat_of_selected_atoms(tiny_inputs):
+    # rows of a subset of atoms equal the same rows of the whole system
+    x = tiny_inputs["tiny_alloy"]
+    c = x.cfg
+    full = ev.env_mat(x.coords, c.box, x.atype, x.nlist, c.rc, c.rcs, *_stats(x))
+    atoms = np.array([3, 0, 11])
+    part = ev.env_mat(x.coords, c.box, x.atype[atoms], x.nlist[atoms], c.rc, c.rcs, *_stats(x), atoms=atoms)
+    assert np.array_equal(part, full[atoms])
