@@ -158,6 +158,79 @@ def bench_descriptor_bwd(args):
     print(json.dumps(res), flush=True)
 
 
+def bench_env_force(args):
+    """The steps on either side of the descriptor: dpc_env_mat_a (positions ->
+    R~) and dpc_force_a (dE/dR~ -> forces, virials) over the configuration,
+    with the reverse slots built once (as a neighbour list is).  dE/dR~ is
+    seeded standard normal on valid slots.  Both kernels are bound by HBM:
+    env 4 B (nlist) + 32 B (R~) per slot; force 4 + 4 (nlist, reverse slot)
+    + 32 (own dE/dR~ row) per slot + 32 (the reverse row) per valid slot +
+    96 B (F, V) per atom, float64."""
+    import numpy as np
+    import torch
+    import paper_2107_02103_amd as P
+    from synth import make_inputs
+    from synth.configs import get_config
+    from synth.system import random_grad
+
+    key = int(args.config) if args.config.isdigit() else args.config
+    cfg = get_config(key)
+    log(f"[bench] env/force: generating {cfg.name}")
+    x = make_inputs(cfg, with_grad=False)
+    n, nnei, pairs = cfg.natoms, cfg.nnei, x.n_valid
+    st = x.stats
+    coord = torch.from_numpy(x.coords).cuda()
+    at = torch.from_numpy(x.atype).cuda()
+    nl = torch.from_numpy(x.nlist).cuda()
+    em = torch.empty((n, nnei, 4), dtype=torch.float64, device="cuda")
+    rev = torch.empty((n, nnei), dtype=torch.int32, device="cuda")
+    lam = random_grad(np.random.default_rng([2107_02103, 88, 9]), n, nnei) * (x.nlist >= 0)[..., None]
+    dem = torch.from_numpy(lam).cuda()
+    del lam
+    F = torch.empty((n, 3), dtype=torch.float64, device="cuda")
+    V = torch.empty((n, 9), dtype=torch.float64, device="cuda")
+    s = torch.cuda.Stream()
+    env = lambda: P.dpc_env_mat_a(s, P.DPC_F64, n, cfg.ntypes, nnei, cfg.box, cfg.rc, cfg.rcs,
+                                  st["mean"], st["sigma"], st["sigma_all"], coord, at, nl, em)
+    force = lambda: P.dpc_force_a(s, P.DPC_F64, n, cfg.ntypes, nnei, cfg.box, cfg.rc, cfg.rcs,
+                                  st["sigma"], st["sigma_all"], coord, at, nl, rev, dem, F, V)
+    with torch.cuda.stream(s):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        P.dpc_nlist_reverse(s, n, cfg.ntypes, cfg.sel, cfg.box, coord, at, nl, rev)
+        e1.record(s)
+        for _ in range(args.warmup):
+            env(); force()
+        torch.cuda.synchronize()
+        rev_ms = e0.elapsed_time(e1)
+        evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(args.steps)]
+        t0 = time.perf_counter()
+        for a, b, c in evs:
+            a.record(s); env(); b.record(s); force(); c.record(s)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+    env_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in evs]))
+    force_ms = float(np.mean([b.elapsed_time(c) for _, b, c in evs]))
+    env_bytes = 36.0 * n * nnei
+    force_bytes = 40.0 * n * nnei + 32.0 * pairs + 96.0 * n
+    dom, dom_ms, dom_bytes = ("force_kernel", force_ms, force_bytes) if force_ms >= env_ms else \
+        ("env_mat_kernel", env_ms, env_bytes)
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    res = {
+        "metric": "environment matrix + force/virial assembly (fp64), neighbour pairs/s + % of HBM bandwidth",
+        "value": pairs * args.steps / wall, "unit": "pairs/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": wall / args.steps * 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {n} atoms, sel {list(cfg.sel)}, rc {cfg.rc}, rcs {cfg.rcs}; "
+                               "dE/dR~ standard normal on valid slots", "atoms": n, "valid_pairs": pairs},
+        "env_ms": env_ms, "force_ms": force_ms, "reverse_ms_once": rev_ms,
+        "env_GBps": env_bytes / (env_ms * 1e-3) / 1e9, "force_GBps": force_bytes / (force_ms * 1e-3) / 1e9,
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": 8000.0, "unit": "GB/s",
+                     "frac": achieved / 8000.0, "traffic": None},
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -170,6 +243,8 @@ def main():
     ap.add_argument("--stride", type=float, default=None,
                     help="table stride d1 on the observed range (band stride 10 x d1; default: the "
                          "workload's 0.01 / 0.1), for the stride study")
+    ap.add_argument("--env-force", action="store_true",
+                    help="time the environment matrix and the force / virial assembly instead")
     ap.add_argument("--descriptor-bwd", action="store_true",
                     help="time the descriptor backward (dE/dT from dE/dD) instead of the se_a step")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -187,6 +262,9 @@ def main():
         return
     if args.descriptor_bwd:
         bench_descriptor_bwd(args)
+        return
+    if args.env_force:
+        bench_env_force(args)
         return
 
     import numpy as np

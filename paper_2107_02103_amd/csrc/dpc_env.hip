@@ -30,6 +30,7 @@ namespace {
 struct EnvGeo {
   int nloc, nnei, ntypes;
   double box, rc, rcs;
+  double inv_box, inv_w;            // 1 / box, 1 / (rc - rcs)
   double mean[DPC_MAX_TYPES], inv_sigma[DPC_MAX_TYPES], inv_sigma_all[DPC_MAX_TYPES];
   int blk[DPC_MAX_TYPES + 1];       // sel block boundaries (slot offsets)
 };
@@ -40,36 +41,42 @@ __device__ __forceinline__ void min_image(const EnvGeo& g, const double* a, cons
 #pragma unroll
   for (int c = 0; c < 3; ++c) {
     const double x = b[c] - a[c];
-    d[c] = x - g.box * round(x / g.box);
+    d[c] = x - g.box * round(x * g.inv_box);
   }
 }
 
 // s(r) and ds/dr of Eq. (1)
 __device__ __forceinline__ void weight(const EnvGeo& g, double r, double& s, double& ds) {
+  const double ir = 1.0 / r;
   if (r < g.rcs) {
-    s = 1.0 / r;
-    ds = -s * s;
+    s = ir;
+    ds = -ir * ir;
   } else if (r < g.rc) {
-    const double w = g.rc - g.rcs, u = (r - g.rcs) / w;
+    const double u = (r - g.rcs) * g.inv_w;
     const double u2 = u * u, u3 = u2 * u;
     const double sw = u3 * (-6.0 * u2 + 15.0 * u - 10.0) + 1.0;
-    const double dsw = (-30.0 * u2 * (u - 1.0) * (u - 1.0)) / w;
-    s = sw / r;
-    ds = dsw / r - sw / (r * r);
+    const double dsw = (-30.0 * u2 * (u - 1.0) * (u - 1.0)) * g.inv_w;
+    s = sw * ir;
+    ds = (dsw - sw * ir) * ir;
   } else {
     s = 0.0;
     ds = 0.0;
   }
 }
 
-template <typename TO>
-__global__ __launch_bounds__(256) void env_mat_kernel(const EnvGeo g, const double* __restrict__ coord,
+// workgroup b covers slots 256 c .. 256 c + 255 of atom b / chunks (c = b mod
+// chunks), so that the atom index is uniform; rows are written 16 bytes at a
+// time when the output is 16-byte aligned (kPair)
+template <typename TO, bool kPair>
+__global__ __launch_bounds__(256) void env_mat_kernel(const EnvGeo g, int chunks,
+                                                      const double* __restrict__ coord,
                                                       const int* __restrict__ atype,
                                                       const int* __restrict__ nlist,
                                                       TO* __restrict__ em) {
-  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= (int64_t)g.nloc * g.nnei) return;
-  const int i = (int)(e / g.nnei);
+  const int i = __builtin_amdgcn_readfirstlane((int)(blockIdx.x / (unsigned)chunks));
+  const int s = (int)(blockIdx.x - (unsigned)i * chunks) * 256 + threadIdx.x;
+  if (s >= g.nnei) return;
+  const size_t e = (size_t)i * g.nnei + s;
   const int j = __builtin_nontemporal_load(nlist + e);
   double row[4] = {0.0, 0.0, 0.0, 0.0};
   const int t = atype[i];
@@ -77,10 +84,10 @@ __global__ __launch_bounds__(256) void env_mat_kernel(const EnvGeo g, const doub
     double d[3];
     min_image(g, coord + 3 * (size_t)i, coord + 3 * (size_t)j, d);
     const double r = sqrt(d[0] * d[0] + d[1] * d[1] + d[2] * d[2]);
-    double s, ds;
-    weight(g, r, s, ds);
-    row[0] = (s - g.mean[t]) * g.inv_sigma[t];
-    const double f = s * g.inv_sigma_all[t];
+    double sv, ds;
+    weight(g, r, sv, ds);
+    row[0] = (sv - g.mean[t]) * g.inv_sigma[t];
+    const double f = sv * g.inv_sigma_all[t];
     row[1] = f * d[0];
     row[2] = f * d[1];
     row[3] = f * d[2];
@@ -88,8 +95,18 @@ __global__ __launch_bounds__(256) void env_mat_kernel(const EnvGeo g, const doub
     row[0] = row[1] = row[2] = row[3] = (double)NAN;
   }
   TO* o = em + 4 * e;
+  if constexpr (kPair && sizeof(TO) == 8) {
+    typedef double D2 __attribute__((ext_vector_type(2)));
+    __builtin_nontemporal_store(D2{row[0], row[1]}, reinterpret_cast<D2*>(o));
+    __builtin_nontemporal_store(D2{row[2], row[3]}, reinterpret_cast<D2*>(o) + 1);
+  } else if constexpr (kPair) {
+    typedef float F4 __attribute__((ext_vector_type(4)));
+    __builtin_nontemporal_store(F4{(float)row[0], (float)row[1], (float)row[2], (float)row[3]},
+                                reinterpret_cast<F4*>(o));
+  } else {
 #pragma unroll
-  for (int c = 0; c < 4; ++c) __builtin_nontemporal_store((TO)row[c], o + c);
+    for (int c = 0; c < 4; ++c) __builtin_nontemporal_store((TO)row[c], o + c);
+  }
 }
 
 // rev[i][s] = slot of i in the list of j = nlist[i][s] (in the sel block of
@@ -236,6 +253,8 @@ int make_env_geo(int nloc, int ntypes, int nnei, double box, double rc, double r
   g->box = box;
   g->rc = rc;
   g->rcs = rcs;
+  g->inv_box = 1.0 / box;
+  g->inv_w = 1.0 / (rc - rcs);
   for (int t = 0; t < DPC_MAX_TYPES; ++t) {
     g->mean[t] = 0.0;
     g->inv_sigma[t] = g->inv_sigma_all[t] = 0.0;
@@ -279,14 +298,22 @@ extern "C" int dpc_env_mat_a(void* stream, dpc_dtype dtype, int nloc, int ntypes
   if (st != DPC_OK) return st;
   if (nloc == 0) return DPC_OK;
   if (!coord || !atype || !nlist || !em) return DPC_EINVAL;
-  dim3 grid;
-  if (slot_grid(g, &grid) != DPC_OK) return DPC_ENOTSUP;
+  const int chunks = (nnei + 255) / 256;
+  if ((int64_t)nloc * chunks >= (int64_t(1) << 31)) return DPC_ENOTSUP;
+  const dim3 grid((unsigned)(nloc * chunks));
+  const bool pair = reinterpret_cast<uintptr_t>(em) % 16 == 0;
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();  // report only what this launch raises
-  if (dtype == DPC_F64)
-    hipLaunchKernelGGL(env_mat_kernel<double>, grid, dim3(256), 0, s, g, coord, atype, nlist, (double*)em);
-  else
-    hipLaunchKernelGGL(env_mat_kernel<float>, grid, dim3(256), 0, s, g, coord, atype, nlist, (float*)em);
+  auto go = [&](auto kern, auto* out) {
+    hipLaunchKernelGGL(kern, grid, dim3(256), 0, s, g, chunks, coord, atype, nlist, out);
+  };
+  if (dtype == DPC_F64) {
+    if (pair) go(env_mat_kernel<double, true>, (double*)em);
+    else go(env_mat_kernel<double, false>, (double*)em);
+  } else {
+    if (pair) go(env_mat_kernel<float, true>, (float*)em);
+    else go(env_mat_kernel<float, false>, (float*)em);
+  }
   return dpc_internal_launch_status();
 }
 
