@@ -32,7 +32,9 @@ def log(*a):
 
 
 def kernel_source_hash(kernel="se_a"):
-    src = "dpc_descriptor.hip" if kernel.startswith("descriptor") else "dpc_se_a.hip"
+    src = ("dpc_descriptor.hip" if kernel.startswith("descriptor") else
+           "dpc_env.hip" if kernel in ("env_mat_kernel", "force_kernel", "reverse_kernel") else
+           "dpc_se_a.hip")
     p = os.path.join(ROOT, "paper_2107_02103_amd", "csrc", src)
     return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
 
@@ -226,7 +228,7 @@ def bench_env_force(args):
         "env_ms": env_ms, "force_ms": force_ms, "reverse_ms_once": rev_ms,
         "env_GBps": env_bytes / (env_ms * 1e-3) / 1e9, "force_GBps": force_bytes / (force_ms * 1e-3) / 1e9,
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": 8000.0, "unit": "GB/s",
-                     "frac": achieved / 8000.0, "traffic": None},
+                     "frac": achieved / 8000.0, "traffic": hbm_traffic(cfg.name, dom)},
     }
     print(json.dumps(res), flush=True)
 
