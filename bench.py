@@ -233,6 +233,82 @@ def bench_env_force(args):
     print(json.dumps(res), flush=True)
 
 
+def bench_chain(args):
+    """Positions to forces with everything but the fitting net: dpc_env_mat_a
+    (R~), dpc_se_a_tab_fwd (T, D), dpc_descriptor_bwd (dE/dT from a seeded
+    standard-normal dE/dD, standing in for the fitting net's gradient),
+    dpc_se_a_tab_bwd (dE/dR~) and dpc_force_a, one launch each per step on
+    one stream, the reverse slots built once.  float64."""
+    import numpy as np
+    import torch
+    import paper_2107_02103_amd as P
+    from synth import make_inputs
+    from synth.configs import get_config
+    from synth.system import random_grad
+
+    key = int(args.config) if args.config.isdigit() else args.config
+    cfg = get_config(key)
+    log(f"[bench] chain: generating {cfg.name}")
+    x = make_inputs(cfg, with_grad=False)
+    n, nnei, m1, m2, pairs = cfg.natoms, cfg.nnei, cfg.m1, cfg.m2, x.n_valid
+    st = x.stats
+    op = P.SeATab(x.nets, x.lo, x.L1, x.L2, cfg.d1, cfg.d2, cfg.sel, m2)
+    coord = torch.from_numpy(x.coords).cuda()
+    at = torch.from_numpy(x.atype).cuda()
+    nl = torch.from_numpy(x.nlist).cuda()
+    dD = torch.from_numpy(random_grad(np.random.default_rng([2107_02103, 77, 5]), n, m1, width=m2)).cuda()
+    em = torch.empty((n, nnei, 4), dtype=torch.float64, device="cuda")
+    T = torch.empty((n, m1, 4), dtype=torch.float64, device="cuda")
+    D = torch.empty((n, m1, m2), dtype=torch.float64, device="cuda")
+    dT = torch.empty_like(T)
+    dR = torch.empty_like(em)
+    rev = torch.empty((n, nnei), dtype=torch.int32, device="cuda")
+    F = torch.empty((n, 3), dtype=torch.float64, device="cuda")
+    V = torch.empty((n, 9), dtype=torch.float64, device="cuda")
+    s = torch.cuda.Stream()
+    names = ["env", "fwd", "descriptor_bwd", "bwd", "force"]
+
+    def step(evs=None):
+        calls = [
+            lambda: P.dpc_env_mat_a(s, P.DPC_F64, n, cfg.ntypes, nnei, cfg.box, cfg.rc, cfg.rcs, st["mean"],
+                                    st["sigma"], st["sigma_all"], coord, at, nl, em),
+            lambda: op.forward(em, nl, at, T, D, stream=s),
+            lambda: op.descriptor_backward(T, dD, dT, stream=s),
+            lambda: op.backward(em, nl, at, dT, dR, stream=s),
+            lambda: P.dpc_force_a(s, P.DPC_F64, n, cfg.ntypes, nnei, cfg.box, cfg.rc, cfg.rcs, st["sigma"],
+                                  st["sigma_all"], coord, at, nl, rev, dR, F, V),
+        ]
+        for k, c in enumerate(calls):
+            if evs is not None:
+                evs[k].record(s)
+            c()
+        if evs is not None:
+            evs[-1].record(s)
+
+    with torch.cuda.stream(s):
+        P.dpc_nlist_reverse(s, n, cfg.ntypes, cfg.sel, cfg.box, coord, at, nl, rev)
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+        t0 = time.perf_counter()
+        for e in evs:
+            step(e)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+    per = {nm: float(np.mean([e[k].elapsed_time(e[k + 1]) for e in evs])) for k, nm in enumerate(names)}
+    res = {
+        "metric": "positions to forces without the fitting net (fp64), neighbour pairs/s",
+        "value": pairs * args.steps / wall, "unit": "pairs/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": wall / args.steps * 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {n} atoms, sel {list(cfg.sel)}; dE/dD standard normal",
+                   "atoms": n, "valid_pairs": pairs},
+        "kernel_ms": per,
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -245,6 +321,8 @@ def main():
     ap.add_argument("--stride", type=float, default=None,
                     help="table stride d1 on the observed range (band stride 10 x d1; default: the "
                          "workload's 0.01 / 0.1), for the stride study")
+    ap.add_argument("--chain", action="store_true",
+                    help="time positions -> R~ -> T, D -> dE/dT -> dE/dR~ -> forces (no fitting net)")
     ap.add_argument("--env-force", action="store_true",
                     help="time the environment matrix and the force / virial assembly instead")
     ap.add_argument("--descriptor-bwd", action="store_true",
@@ -267,6 +345,9 @@ def main():
         return
     if args.env_force:
         bench_env_force(args)
+        return
+    if args.chain:
+        bench_chain(args)
         return
 
     import numpy as np

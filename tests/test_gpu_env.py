@@ -181,3 +181,39 @@ def test_force_properties_at_size(key):
     tot = np.abs(F.sum(0)).max()
     print(f"[gpu-env] {x.cfg.name} |sum F| {tot:.2e}, max |F| {np.abs(F).max():.2e}", flush=True)
     assert tot <= 1e-10 * np.abs(F).max() * np.sqrt(len(F))
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("key", ["tiny_water", "tiny_alloy", 0])
+def test_chain_positions_to_forces(key):
+    # GPU: env matrix -> forward -> descriptor backward -> backward -> forces,
+    # against the oracle's same chain (float64)
+    import paper_2107_02103_amd as P
+    from oracle.se_a import backward, descriptor_backward, forward
+    from oracle.table import build_tables
+    x = _inputs(key)
+    c = x.cfg
+    mean, sigma, sigma_all = _stats(x)
+    n = len(x.atype)
+    W = random_grad(np.random.default_rng([2107_02103, 99, 1]), n, c.m1, width=c.m2)
+    op = P.SeATab(x.nets, x.lo, x.L1, x.L2, c.d1, c.d2, c.sel, c.m2)
+    coord, at, nl = _dev(x)
+    em = torch.empty((n, c.nnei, 4), dtype=torch.float64, device="cuda")
+    P.dpc_env_mat_a(torch.cuda.current_stream(), P.DPC_F64, n, c.ntypes, c.nnei, c.box, c.rc, c.rcs,
+                    mean, sigma, sigma_all, coord, at, nl, em)
+    T, D = op.forward(em, nl, at)
+    dT = op.descriptor_backward(T, torch.from_numpy(W).cuda())
+    dR = op.backward(em, nl, at, dT)
+    rev = _reverse_gpu(x)
+    F = torch.empty((n, 3), dtype=torch.float64, device="cuda")
+    P.dpc_force_a(torch.cuda.current_stream(), P.DPC_F64, n, c.ntypes, c.nnei, c.box, c.rc, c.rcs,
+                  sigma, sigma_all, coord, at, nl, rev, dR, F, None)
+    torch.cuda.synchronize()
+    tabs = build_tables(x)
+    emr = ev.env_mat(x.coords, c.box, x.atype, x.nlist, c.rc, c.rcs, mean, sigma, sigma_all)
+    Tr, _ = forward(emr, x.nlist, x.atype, tabs, c.sel, c.m2)
+    dRr = backward(emr, x.nlist, x.atype, tabs, c.sel, descriptor_backward(Tr, W))
+    Fr, _ = ev.force_virial(x.coords, c.box, x.atype, x.nlist, c.rc, c.rcs, mean, sigma, sigma_all, dRr)
+    err = _normwise(F.cpu().numpy(), Fr)
+    print(f"[gpu-env] {c.name} chain forces normwise {err:.2e}", flush=True)
+    assert err <= 1e-10

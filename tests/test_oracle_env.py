@@ -123,3 +123,32 @@ def test_env_mat_of_selected_atoms(tiny_inputs):
     atoms = np.array([3, 0, 11])
     part = ev.env_mat(x.coords, c.box, x.atype[atoms], x.nlist[atoms], c.rc, c.rcs, *_stats(x), atoms=atoms)
     assert np.array_equal(part, full[atoms])
+
+
+def test_chain_positions_to_forces(tiny_inputs):
+    # E = <W, D(T(R~(r)))>: forces from the oracle's chain (descriptor
+    # backward, backward, force assembly) against central differences of E
+    # in the positions
+    from oracle.se_a import backward, descriptor_backward, forward
+    from oracle.table import build_tables
+    x = tiny_inputs["tiny_water"]
+    c = x.cfg
+    tabs = build_tables(x)
+    mean, sigma, sigma_all = _stats(x)
+
+    def energy(coords, W):
+        em = ev.env_mat(coords, c.box, x.atype, x.nlist, c.rc, c.rcs, mean, sigma, sigma_all)
+        _, D = forward(em, x.nlist, x.atype, tabs, c.sel, c.m2)
+        return float(np.sum(W * D)), em
+    W = np.random.default_rng(7).normal(size=(len(x.atype), c.m1, c.m2))
+    _, em = energy(x.coords, W)
+    T, _ = forward(em, x.nlist, x.atype, tabs, c.sel, c.m2)
+    dR = backward(em, x.nlist, x.atype, tabs, c.sel, descriptor_backward(T, W))
+    F, _ = ev.force_virial(x.coords, c.box, x.atype, x.nlist, c.rc, c.rcs, mean, sigma, sigma_all, dR)
+    h = 1e-6
+    for i in (0, 5):
+        for a in range(3):
+            cp = x.coords.copy(); cm = x.coords.copy()
+            cp[i, a] += h; cm[i, a] -= h
+            fd = -(energy(cp, W)[0] - energy(cm, W)[0]) / (2 * h)
+            assert abs(fd - F[i, a]) <= 1e-5 * np.max(np.abs(F[i])), (i, a, fd, F[i, a])
