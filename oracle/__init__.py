@@ -14,7 +14,8 @@ arXiv:2107.02103, Sec. II) in float64:
 * ``cref``  -- the same forward/backward as plain C loops (OpenMP over atoms)
                for the large workloads;
 * ``env``   -- the environment matrix R~ from positions (Eq. (1) and the
-               normalisation) and the forces and virials from dE/dR~.
+               normalisation) and the forces and virials from dE/dR~;
+* ``fitting`` -- the fitting net D -> E and its backward dE/dD.
 
 It is test infrastructure only: the tests, ``__graft_entry__.smoke()`` and the
 ``cpu_baseline`` leg of ``bench.py`` may use it; the product path never does.

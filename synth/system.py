@@ -217,6 +217,19 @@ def _chunk(cfg, basis, types, disp, sel, sel_off, cand, b, c0, c1, nlist, em):
     return stats, smax, int(ok.sum())
 
 
+def random_fitting_net(rng, n_in, widths=(240, 240, 240)):
+    """Fitting-net weights (descriptor -> energy): hidden layers W_l ~
+    N(0, 1/fan_in), b_l ~ N(0, 1); output w_out ~ N(0, 1/width), b_out ~ N(0, 1)."""
+    W, b = [], []
+    fan = n_in
+    for w in widths:
+        W.append(rng.normal(0.0, 1.0 / np.sqrt(fan), size=(fan, w)))
+        b.append(rng.normal(0.0, 1.0, size=(w,)))
+        fan = w
+    return {"W": W, "b": b, "w_out": rng.normal(0.0, 1.0 / np.sqrt(fan), size=(fan,)),
+            "b_out": float(rng.normal(0.0, 1.0))}
+
+
 def random_grad(rng, nat, m1, threads=None, chunk=65536, width=4):
     """dE/dT ~ N(0, 1) of shape [nat, m1, width] (width 4: dE/dT; width M':
     dE/dD, or a T-shaped input of the descriptor backward), drawn in fixed
