@@ -233,12 +233,76 @@ def bench_env_force(args):
     print(json.dumps(res), flush=True)
 
 
+def _fitting_setup(n, m1, m2, width=240):
+    """A seeded random fitting net on the device, its workspace and a rocBLAS handle."""
+    import numpy as np
+    import torch
+    import paper_2107_02103_amd as P
+    from synth.system import random_fitting_net
+    net = random_fitting_net(np.random.default_rng([2107_02103, 66, 1]), m1 * m2, (width,) * 3)
+    keep = [torch.from_numpy(np.ascontiguousarray(a)).cuda() for a in net["W"] + net["b"] + [net["w_out"]]]
+    c = P.dpc_fitting_net()
+    c.n_in, c.width, c.b_out = m1 * m2, width, net["b_out"]
+    for l in range(3):
+        c.W[l] = keep[l].data_ptr()
+        c.b[l] = keep[3 + l].data_ptr()
+    c.w_out = keep[6].data_ptr()
+    nb = P.dpc_fitting_workspace_bytes(n, width)
+    ws = torch.empty(nb // 8, dtype=torch.float64, device="cuda")
+    return c, keep, ws, nb, P.RocblasHandle()
+
+
+def bench_fitting(args):
+    """dpc_fitting_fwd_bwd (energy and dE/dD) over the configuration's atoms:
+    M = 100, M' = 16 descriptors (seeded standard normal), widths 240; its
+    GEMMs run on the matrix cores through rocBLAS.  FLOP per atom:
+    4 (1600 x 240 + 2 x 240 x 240) (forward and data gradient)."""
+    import numpy as np
+    import torch
+    import paper_2107_02103_amd as P
+    from synth.configs import get_config
+    from synth.system import random_grad
+    key = int(args.config) if args.config.isdigit() else args.config
+    cfg = get_config(key)
+    n, m1, m2 = cfg.natoms, cfg.m1, cfg.m2
+    log(f"[bench] fitting net: {n} atoms")
+    D = torch.from_numpy(random_grad(np.random.default_rng([2107_02103, 77, 8]), n, m1, width=m2)).cuda()
+    net, keep, ws, nb, h = _fitting_setup(n, m1, m2)
+    E = torch.empty(n, dtype=torch.float64, device="cuda")
+    G = torch.empty_like(D)
+    s = torch.cuda.Stream()
+    run = lambda: P.dpc_fitting_fwd_bwd(s, h.value, n, net, D, ws, nb, E, G)
+    with torch.cuda.stream(s):
+        for _ in range(args.warmup):
+            run()
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        t0 = time.perf_counter()
+        for a, b in evs:
+            a.record(s); run(); b.record(s)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+    ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    flop = 4.0 * n * (m1 * m2 * 240 + 2 * 240 * 240)
+    res = {"metric": "fitting net energy + dE/dD (fp64), atoms/s + % of FP64 matrix peak",
+           "value": n * args.steps / wall, "unit": "atoms/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": wall / args.steps * 1e3, "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+           "config": {"workload": f"{cfg.name} fitting net: {n} atoms, input {m1 * m2}, widths 240-240-240, "
+                                  "descriptors standard normal", "atoms": n},
+           "ms": ms,
+           "roofline": {"bound": "mfma", "kernel": "rocBLAS dgemm + fitting kernels", "achieved": flop / (ms * 1e-3) / 1e12,
+                        "peak": 78.6, "unit": "TFLOP/s", "frac": flop / (ms * 1e-3) / 1e12 / 78.6, "traffic": None}}
+    h.close()
+    print(json.dumps(res), flush=True)
+
+
 def bench_chain(args):
-    """Positions to forces with everything but the fitting net: dpc_env_mat_a
-    (R~), dpc_se_a_tab_fwd (T, D), dpc_descriptor_bwd (dE/dT from a seeded
-    standard-normal dE/dD, standing in for the fitting net's gradient),
-    dpc_se_a_tab_bwd (dE/dR~) and dpc_force_a, one launch each per step on
-    one stream, the reverse slots built once.  float64."""
+    """Positions to energies and forces: dpc_env_mat_a (R~), dpc_se_a_tab_fwd
+    (T, D), dpc_fitting_fwd_bwd (E, dE/dD; seeded random fitting net),
+    dpc_descriptor_bwd (dE/dT), dpc_se_a_tab_bwd (dE/dR~) and dpc_force_a,
+    one call each per step on one stream, the reverse slots built once.
+    float64."""
     import numpy as np
     import torch
     import paper_2107_02103_amd as P
@@ -256,7 +320,9 @@ def bench_chain(args):
     coord = torch.from_numpy(x.coords).cuda()
     at = torch.from_numpy(x.atype).cuda()
     nl = torch.from_numpy(x.nlist).cuda()
-    dD = torch.from_numpy(random_grad(np.random.default_rng([2107_02103, 77, 5]), n, m1, width=m2)).cuda()
+    fnet, keep, ws, nb, hblas = _fitting_setup(n, m1, m2)
+    Ea = torch.empty(n, dtype=torch.float64, device="cuda")
+    dD = torch.empty((n, m1, m2), dtype=torch.float64, device="cuda")
     em = torch.empty((n, nnei, 4), dtype=torch.float64, device="cuda")
     T = torch.empty((n, m1, 4), dtype=torch.float64, device="cuda")
     D = torch.empty((n, m1, m2), dtype=torch.float64, device="cuda")
@@ -266,13 +332,14 @@ def bench_chain(args):
     F = torch.empty((n, 3), dtype=torch.float64, device="cuda")
     V = torch.empty((n, 9), dtype=torch.float64, device="cuda")
     s = torch.cuda.Stream()
-    names = ["env", "fwd", "descriptor_bwd", "bwd", "force"]
+    names = ["env", "fwd", "fitting", "descriptor_bwd", "bwd", "force"]
 
     def step(evs=None):
         calls = [
             lambda: P.dpc_env_mat_a(s, P.DPC_F64, n, cfg.ntypes, nnei, cfg.box, cfg.rc, cfg.rcs, st["mean"],
                                     st["sigma"], st["sigma_all"], coord, at, nl, em),
             lambda: op.forward(em, nl, at, T, D, stream=s),
+            lambda: P.dpc_fitting_fwd_bwd(s, hblas.value, n, fnet, D, ws, nb, Ea, dD),
             lambda: op.descriptor_backward(T, dD, dT, stream=s),
             lambda: op.backward(em, nl, at, dT, dR, stream=s),
             lambda: P.dpc_force_a(s, P.DPC_F64, n, cfg.ntypes, nnei, cfg.box, cfg.rc, cfg.rcs, st["sigma"],
@@ -290,7 +357,7 @@ def bench_chain(args):
         for _ in range(args.warmup):
             step()
         torch.cuda.synchronize()
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(args.steps)]
         t0 = time.perf_counter()
         for e in evs:
             step(e)
@@ -298,11 +365,11 @@ def bench_chain(args):
         wall = time.perf_counter() - t0
     per = {nm: float(np.mean([e[k].elapsed_time(e[k + 1]) for e in evs])) for k, nm in enumerate(names)}
     res = {
-        "metric": "positions to forces without the fitting net (fp64), neighbour pairs/s",
+        "metric": "positions to energies and forces (fp64), neighbour pairs/s",
         "value": pairs * args.steps / wall, "unit": "pairs/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": wall / args.steps * 1e3, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: {n} atoms, sel {list(cfg.sel)}; dE/dD standard normal",
+        "config": {"workload": f"{cfg.name}: {n} atoms, sel {list(cfg.sel)}; random fitting net 240-240-240",
                    "atoms": n, "valid_pairs": pairs},
         "kernel_ms": per,
     }
@@ -322,7 +389,8 @@ def main():
                     help="table stride d1 on the observed range (band stride 10 x d1; default: the "
                          "workload's 0.01 / 0.1), for the stride study")
     ap.add_argument("--chain", action="store_true",
-                    help="time positions -> R~ -> T, D -> dE/dT -> dE/dR~ -> forces (no fitting net)")
+                    help="time positions -> R~ -> T, D -> E, dE/dD -> dE/dT -> dE/dR~ -> forces")
+    ap.add_argument("--fitting", action="store_true", help="time the fitting net (energy and dE/dD)")
     ap.add_argument("--env-force", action="store_true",
                     help="time the environment matrix and the force / virial assembly instead")
     ap.add_argument("--descriptor-bwd", action="store_true",
@@ -348,6 +416,9 @@ def main():
         return
     if args.chain:
         bench_chain(args)
+        return
+    if args.fitting:
+        bench_fitting(args)
         return
 
     import numpy as np

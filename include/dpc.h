@@ -219,6 +219,36 @@ int dpc_force_a(void* stream, dpc_dtype dtype, int nloc, int ntypes, int nnei, d
                 const double* coord, const int* atype, const int* nlist, const int* rev,
                 const void* dE_dem, double* force, double* virial);
 
+/* Fitting net (paper Sec. II: a fully connected network maps the descriptor
+ * D_i to the atomic energy E_i; Sec. III: widths (240, 240, 240)), read as
+ *   h_1 = tanh(x W_1 + b_1),  h_l = h_{l-1} + tanh(h_{l-1} W_l + b_l) (l = 2, 3),
+ *   E_i = h_3 . w_out + b_out,   x = D_i flattened row-major (n_in = m1 * m2),
+ * with its backward dE_i/dD_i (the dE_dD input of dpc_descriptor_bwd).
+ * Weights are device float64, row-major: W[0] [n_in][width], W[1], W[2]
+ * [width][width], b[l] [width], w_out [width]; the three widths are equal.  */
+typedef struct {
+  int n_in, width;
+  const double* W[3];
+  const double* b[3];
+  const double* w_out;
+  double b_out;
+} dpc_fitting_net;
+
+/* Bytes of device workspace dpc_fitting_fwd_bwd needs: 6 nloc width float64
+ * (the three layers' tanh outputs and three working arrays). 0 for bad sizes. */
+size_t dpc_fitting_workspace_bytes(int nloc, int width);
+
+/* E [nloc] and, if dE_dD is not NULL, dE/dD [nloc][n_in] (float64) for
+ * D [nloc][n_in] (float64, device).  The layer products run as rocBLAS
+ * double-precision GEMMs on the caller's handle `blas` (a rocblas_handle as
+ * void*; its stream is set to `stream`, and its pointer mode must be host);
+ * the library allocates nothing: `workspace` (device, 16-byte aligned,
+ * >= dpc_fitting_workspace_bytes) is the caller's.  Sums have a fixed order
+ * for a given rocBLAS.  DPC_EHIP reports a HIP or rocBLAS failure.          */
+int dpc_fitting_fwd_bwd(void* stream, void* blas, int nloc, const dpc_fitting_net* net,
+                        const double* D, void* workspace, size_t workspace_bytes, double* E,
+                        double* dE_dD);
+
 #ifdef __cplusplus
 }
 #endif

@@ -33,7 +33,7 @@ DPC_F64, DPC_F32, DPC_F32_ACC64 = 0, 1, 2
 DPC_MAX_TYPES, DPC_MAX_M1 = 8, 256
 EXPORTED = ("dpc_strerror", "dpc_last_hip_error", "dpc_version", "dpc_table_layout", "dpc_build_table",
             "dpc_se_a_tab_fwd", "dpc_se_a_tab_bwd", "dpc_descriptor_bwd", "dpc_env_mat_a",
-            "dpc_nlist_reverse", "dpc_force_a")
+            "dpc_nlist_reverse", "dpc_force_a", "dpc_fitting_workspace_bytes", "dpc_fitting_fwd_bwd")
 
 
 class dpc_range(C.Structure):
@@ -63,6 +63,16 @@ _lib.dpc_se_a_tab_bwd.restype = C.c_int
 _lib.dpc_se_a_tab_bwd.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.POINTER(C.c_int),
                                   C.c_int, C.POINTER(dpc_range), C.c_void_p, C.c_void_p,
                                   C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+class dpc_fitting_net(C.Structure):
+    _fields_ = [("n_in", C.c_int), ("width", C.c_int), ("W", C.c_void_p * 3), ("b", C.c_void_p * 3),
+                ("w_out", C.c_void_p), ("b_out", C.c_double)]
+
+
+_lib.dpc_fitting_workspace_bytes.restype = C.c_size_t
+_lib.dpc_fitting_workspace_bytes.argtypes = [C.c_int, C.c_int]
+_lib.dpc_fitting_fwd_bwd.restype = C.c_int
+_lib.dpc_fitting_fwd_bwd.argtypes = [C.c_void_p, C.c_void_p, C.c_int, C.POINTER(dpc_fitting_net),
+                                     C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p, C.c_void_p]
 _D = C.c_double
 _lib.dpc_env_mat_a.restype = C.c_int
 _lib.dpc_env_mat_a.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_int, _D, _D, _D,
@@ -262,3 +272,41 @@ def dpc_force_a(stream, dtype, nloc, ntypes, nnei, box, rc, rcs, sigma, sigma_al
                             _ptr(rev, name="rev"), _ptr(dE_dem, name="dE_dem"),
                             _ptr(force, name="force"), _ptr(virial, name="virial")),
            "dpc_force_a")
+
+
+def dpc_fitting_workspace_bytes(nloc, width):
+    return int(_lib.dpc_fitting_workspace_bytes(int(nloc), int(width)))
+
+
+def dpc_fitting_fwd_bwd(stream, blas, nloc, net, D, workspace, workspace_bytes, E, dE_dD=None):
+    """``net``: a dpc_fitting_net whose pointers are device addresses;
+    ``blas``: a rocblas_handle (int), see RocblasHandle."""
+    _check(_lib.dpc_fitting_fwd_bwd(_stream(stream), blas, int(nloc), C.byref(net), _ptr(D, name="D"),
+                                    _ptr(workspace, name="workspace"), int(workspace_bytes),
+                                    _ptr(E, name="E"), _ptr(dE_dD, name="dE_dD")),
+           "dpc_fitting_fwd_bwd")
+
+
+class RocblasHandle:
+    """A rocBLAS handle for dpc_fitting_fwd_bwd, created and destroyed through
+    librocblas (the caller owns it; the library only sets its stream)."""
+
+    def __init__(self):
+        self._rb = C.CDLL("librocblas.so.5")
+        self._rb.rocblas_create_handle.argtypes = [C.POINTER(C.c_void_p)]
+        self._rb.rocblas_destroy_handle.argtypes = [C.c_void_p]
+        h = C.c_void_p()
+        if self._rb.rocblas_create_handle(C.byref(h)) != 0:
+            raise RuntimeError("rocblas_create_handle failed")
+        self.value = h.value
+
+    def close(self):
+        if self.value:
+            self._rb.rocblas_destroy_handle(C.c_void_p(self.value))
+            self.value = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

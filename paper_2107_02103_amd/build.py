@@ -16,7 +16,7 @@ LIB_DIR = os.path.join(HERE, "_lib")
 LIB = os.path.join(LIB_DIR, "libdpc.so")
 ARCH = "gfx950"
 
-SOURCES = ["dpc_table.cpp", "dpc_se_a.hip", "dpc_descriptor.hip", "dpc_env.hip"]
+SOURCES = ["dpc_table.cpp", "dpc_se_a.hip", "dpc_descriptor.hip", "dpc_env.hip", "dpc_fitting.hip"]
 
 # packed fp32 instructions are disabled for all device code
 HIPCC_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
@@ -43,7 +43,8 @@ def build(verbose=False):
         subprocess.check_call(cmd, stderr=subprocess.STDOUT if not verbose else None)
         objs.append(obj)
     tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs
+    # rocBLAS serves the fitting net's plain GEMMs
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs + ["-lrocblas"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)

@@ -217,3 +217,32 @@ def test_env_entry_points_validate_before_launch():
     P.dpc_env_mat_a(**{**env, "nloc": 0, "coord": 0, "em": 0})
     P.dpc_force_a(**{**f, "nloc": 0, "rev": 0, "force": 0})
     P.dpc_nlist_reverse(0, 0, 2, [4, 4], 20.0, 0, 0, 0, 0)
+
+
+def test_fitting_entry_point_validates_before_launch():
+    fake = 4096
+    assert P.dpc_fitting_workspace_bytes(10, 240) == 6 * 10 * 240 * 8
+    assert P.dpc_fitting_workspace_bytes(-1, 240) == 0
+    net = P.dpc_fitting_net()
+    net.n_in, net.width = 16, 8
+    for l in range(3):
+        net.W[l] = fake
+        net.b[l] = fake
+    net.w_out = fake
+    nb = P.dpc_fitting_workspace_bytes(4, 8)
+    cases = [(dict(nloc=-1), B.DPC_EINVAL), (dict(blas=0), B.DPC_EINVAL), (dict(D=0), B.DPC_EINVAL),
+             (dict(workspace_bytes=nb - 8), B.DPC_EINVAL), (dict(workspace=fake + 8), B.DPC_EINVAL),
+             (dict(E=0), B.DPC_EINVAL)]
+    for kw, code in cases:
+        a = dict(stream=0, blas=fake, nloc=4, net=net, D=fake, workspace=fake, workspace_bytes=nb, E=fake,
+                 dE_dD=None)
+        a.update(kw)
+        with pytest.raises(P.DpcError) as e:
+            P.dpc_fitting_fwd_bwd(**a)
+        assert e.value.status == code, kw
+    net.W[1] = 0
+    with pytest.raises(P.DpcError) as e:
+        P.dpc_fitting_fwd_bwd(0, fake, 4, net, fake, fake, nb, fake)
+    assert e.value.status == B.DPC_EINVAL
+    net.W[1] = fake
+    P.dpc_fitting_fwd_bwd(0, 0, 0, net, 0, 0, 0, 0)                   # nloc = 0: no-op
