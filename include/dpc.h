@@ -234,8 +234,10 @@ typedef struct {
   double b_out;
 } dpc_fitting_net;
 
-/* Bytes of device workspace dpc_fitting_fwd_bwd needs: 6 nloc width float64
- * (the three layers' tanh outputs and three working arrays). 0 for bad sizes. */
+/* Bytes of device workspace dpc_fitting_fwd_bwd needs: five float64 arrays
+ * of nloc * width (rounded up to even) elements: the tanh outputs of layers
+ * 1 and 2, h_2, the pre-activations and the backward accumulator.
+ * 0 for bad sizes.                                                         */
 size_t dpc_fitting_workspace_bytes(int nloc, int width);
 
 /* E [nloc] and, if dE_dD is not NULL, dE/dD [nloc][n_in] (float64) for

@@ -9,9 +9,12 @@
 //
 // The layer products are plain GEMMs with atoms as the long dimension
 // (N x 1600 by 1600 x 240 and 240 x 240, float64) and go to rocBLAS on the
-// caller's handle; bias, tanh, residual, the energy dot product and the
-// backward's (1 - t^2) scaling are the kernels below, each one pass over the
-// activations.  Row-major X [N][c] is column-major [c][N], so
+// caller's handle.  Everything else is four streaming kernels, one pass over
+// the activations each: bias + tanh (layer 1), bias + tanh + residual
+// (layer 2), layer 3 fused with the energy dot product and the first
+// backward scaling (h_3 is never stored), and (1 - t^2) (w_out + e) for the
+// two remaining layers, where e = delta - w_out accumulates in the backward
+// GEMMs so that the constant delta_3 = w_out is never materialised.  Row-major X [N][c] is column-major [c][N], so
 // Z^T = W^T H^T is dgemm(N, N, out, N, in, W, ld out, H, ld in) and
 // dH^T = W dZ^T is dgemm(T, N, in, N, out, W, ld out, dZ, ld out).
 #include <hip/hip_runtime.h>
@@ -24,28 +27,82 @@
 
 namespace {
 
-// t = tanh(z + b) over [n][w]; h = t (first layer) or h += t (residual)
-__global__ __launch_bounds__(256) void bias_tanh_kernel(int64_t n, int w, const double* __restrict__ z,
-                                                        const double* __restrict__ b,
-                                                        double* __restrict__ t, double* __restrict__ h,
-                                                        int residual) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n * w; e += stride) {
-    const double v = tanh(z[e] + b[e % w]);
-    t[e] = v;
-    h[e] = residual ? h[e] + v : v;
+// Grid-stride walk over the element pairs (e, e + 1), e = 0, 2, 4, ... of a
+// row-major [n][w] array, tracking the column of e without a division per
+// step.  nw = n * w may be odd: the last element then goes alone.
+struct PairWalk {
+  int64_t e, step, nw;
+  int col, w, step_col;
+  __device__ PairWalk(int64_t nw_, int w_) : nw(nw_), w(w_) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    step = 2 * (int64_t)gridDim.x * blockDim.x;
+    e = 2 * t;
+    col = (int)(e % w);
+    step_col = (int)(step % w);
+  }
+  __device__ bool ok() const { return e < nw; }
+  __device__ bool pair() const { return e + 1 < nw; }
+  __device__ int col1() const { return col + 1 == w ? 0 : col + 1; }
+  __device__ void next() {
+    e += step;
+    col += step_col;
+    if (col >= w) col -= w;
+  }
+};
+
+__device__ inline double2 ld2(const double* p) { return *reinterpret_cast<const double2*>(p); }
+__device__ inline void st2(double* p, double a, double b) { *reinterpret_cast<double2*>(p) = make_double2(a, b); }
+
+// layer 1: t1 = tanh(z + b1)
+__global__ __launch_bounds__(256) void layer1_kernel(int64_t nw, int w, const double* __restrict__ z,
+                                                     const double* __restrict__ b, double* __restrict__ t1) {
+  for (PairWalk it(nw, w); it.ok(); it.next()) {
+    if (it.pair()) {
+      const double2 v = ld2(z + it.e);
+      st2(t1 + it.e, tanh(v.x + b[it.col]), tanh(v.y + b[it.col1()]));
+    } else {
+      t1[it.e] = tanh(z[it.e] + b[it.col]);
+    }
   }
 }
 
-// E[i] = h[i] . w_out + b_out, one wavefront per atom, fixed-order sum
-__global__ __launch_bounds__(256) void energy_kernel(int n, int w, const double* __restrict__ h,
-                                                     const double* __restrict__ wout, double bout,
-                                                     double* __restrict__ E) {
+// layer 2: t2 = tanh(z + b2), h2 = t1 + t2
+__global__ __launch_bounds__(256) void layer2_kernel(int64_t nw, int w, const double* __restrict__ z,
+                                                     const double* __restrict__ b,
+                                                     const double* __restrict__ t1, double* __restrict__ t2,
+                                                     double* __restrict__ h2) {
+  for (PairWalk it(nw, w); it.ok(); it.next()) {
+    if (it.pair()) {
+      const double2 v = ld2(z + it.e), u = ld2(t1 + it.e);
+      const double a = tanh(v.x + b[it.col]), c = tanh(v.y + b[it.col1()]);
+      st2(t2 + it.e, a, c);
+      st2(h2 + it.e, u.x + a, u.y + c);
+    } else {
+      const double a = tanh(z[it.e] + b[it.col]);
+      t2[it.e] = a;
+      h2[it.e] = t1[it.e] + a;
+    }
+  }
+}
+
+// layer 3 and the energy, one wavefront per atom:
+//   t3 = tanh(z + b3), E = (h2 + t3) . w_out + b_out (fixed-order sum),
+//   and, when dz is given, dz = (1 - t3^2) w_out (dz may alias z)
+__global__ __launch_bounds__(256) void layer3_energy_kernel(int n, int w, const double* z,
+                                                            const double* __restrict__ b,
+                                                            const double* __restrict__ h2,
+                                                            const double* __restrict__ wout, double bout,
+                                                            double* __restrict__ E, double* dz) {
   const int lane = threadIdx.x & 63;
   const int i = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
   if (i >= n) return;
+  const size_t row = (size_t)i * w;
   double acc = 0.0;
-  for (int c = lane; c < w; c += 64) acc = fma(h[(size_t)i * w + c], wout[c], acc);
+  for (int c = lane; c < w; c += 64) {
+    const double t = tanh(z[row + c] + b[c]);
+    acc = fma(h2[row + c] + t, wout[c], acc);
+    if (dz) dz[row + c] = (1.0 - t * t) * wout[c];
+  }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
     const uint64_t u = __builtin_bit_cast(uint64_t, acc);
@@ -56,25 +113,24 @@ __global__ __launch_bounds__(256) void energy_kernel(int n, int w, const double*
   if (lane == 0) E[i] = acc + bout;
 }
 
-// delta[i][c] = w_out[c]
-__global__ __launch_bounds__(256) void delta_init_kernel(int64_t n, int w, const double* __restrict__ wout,
-                                                         double* __restrict__ delta) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n * w; e += stride)
-    delta[e] = wout[e % w];
-}
-
-// dz = (1 - t^2) delta
-__global__ __launch_bounds__(256) void tanh_grad_kernel(int64_t n, const double* __restrict__ t,
-                                                        const double* __restrict__ delta,
+// dz = (1 - t^2) (w_out + e), where e = delta - w_out
+__global__ __launch_bounds__(256) void tanh_grad_kernel(int64_t nw, int w, const double* __restrict__ t,
+                                                        const double* __restrict__ wout,
+                                                        const double* __restrict__ e,
                                                         double* __restrict__ dz) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += stride)
-    dz[e] = (1.0 - t[e] * t[e]) * delta[e];
+  for (PairWalk it(nw, w); it.ok(); it.next()) {
+    if (it.pair()) {
+      const double2 tv = ld2(t + it.e), ev = ld2(e + it.e);
+      st2(dz + it.e, (1.0 - tv.x * tv.x) * (wout[it.col] + ev.x),
+          (1.0 - tv.y * tv.y) * (wout[it.col1()] + ev.y));
+    } else {
+      dz[it.e] = (1.0 - t[it.e] * t[it.e]) * (wout[it.col] + e[it.e]);
+    }
+  }
 }
 
-dim3 stream_grid(int64_t n) {
-  const int64_t b = (n + 255) / 256;
+dim3 stream_grid(int64_t nw) {
+  const int64_t b = (nw / 2 + 255) / 256;
   return dim3((unsigned)(b < 8192 ? (b > 0 ? b : 1) : 8192));
 }
 
@@ -82,7 +138,8 @@ dim3 stream_grid(int64_t n) {
 
 extern "C" size_t dpc_fitting_workspace_bytes(int nloc, int width) {
   if (nloc < 0 || width < 1) return 0;
-  return (size_t)6 * nloc * width * sizeof(double);
+  const size_t nw = (size_t)nloc * width;
+  return 5 * (nw + (nw & 1)) * sizeof(double);   // each array 16-byte aligned
 }
 
 extern "C" int dpc_fitting_fwd_bwd(void* stream, void* blas, int nloc, const dpc_fitting_net* net,
@@ -103,45 +160,39 @@ extern "C" int dpc_fitting_fwd_bwd(void* stream, void* blas, int nloc, const dpc
   if (rocblas_set_stream(hb, s) != rocblas_status_success) return DPC_EHIP;
   const int64_t nw = (int64_t)nloc * w;
   double* ws = static_cast<double*>(workspace);
-  double* t[3] = {ws, ws + nw, ws + 2 * nw};   // tanh outputs of the three layers
-  double* h = ws + 3 * nw;                      // h_2, then h_3
-  double* z = ws + 4 * nw;                      // pre-activations, then dz
-  double* delta = ws + 5 * nw;
+  const int64_t np = nw + (nw & 1);   // array pitch: keeps every array 16-byte aligned
+  double* t1 = ws;            // tanh outputs of layers 1 and 2
+  double* t2 = ws + np;
+  double* h2 = ws + 2 * np;   // h_2 = t_1 + t_2
+  double* z = ws + 3 * np;    // pre-activations, then dz
+  double* e = ws + 4 * np;    // delta_l - w_out in the backward pass
   const double one = 1.0, zero = 0.0;
   (void)hipGetLastError();
   auto gemm_fwd = [&](const double* W, int in, const double* H) {
     return rocblas_dgemm(hb, rocblas_operation_none, rocblas_operation_none, w, nloc, in, &one, W, w,
                          H, in, &zero, z, w) == rocblas_status_success;
   };
-  // layer 1: t_1 = h_1
+  // dH^T = W dZ^T (+ beta C): the data gradient of one layer
+  auto gemm_bwd = [&](const double* W, int in, const double* beta, double* C) {
+    return rocblas_dgemm(hb, rocblas_operation_transpose, rocblas_operation_none, in, nloc, w, &one, W,
+                         w, z, w, beta, C, in) == rocblas_status_success;
+  };
   if (!gemm_fwd(net->W[0], nin, D)) return DPC_EHIP;
-  hipLaunchKernelGGL(bias_tanh_kernel, stream_grid(nw), dim3(256), 0, s, (int64_t)nloc, w, z, net->b[0],
-                     t[0], t[0], 0);
-  // layer 2: h_2 = h_1 + t_2 (h_1 = t_1 copied into h by the first residual step)
-  if (!gemm_fwd(net->W[1], w, t[0])) return DPC_EHIP;
-  if (hipMemcpyAsync(h, t[0], nw * sizeof(double), hipMemcpyDeviceToDevice, s) != hipSuccess)
-    return DPC_EHIP;
-  hipLaunchKernelGGL(bias_tanh_kernel, stream_grid(nw), dim3(256), 0, s, (int64_t)nloc, w, z, net->b[1],
-                     t[1], h, 1);
-  // layer 3: h_3 = h_2 + t_3
-  if (!gemm_fwd(net->W[2], w, h)) return DPC_EHIP;
-  hipLaunchKernelGGL(bias_tanh_kernel, stream_grid(nw), dim3(256), 0, s, (int64_t)nloc, w, z, net->b[2],
-                     t[2], h, 1);
-  hipLaunchKernelGGL(energy_kernel, dim3((nloc + 3) / 4), dim3(256), 0, s, nloc, w, h, net->w_out,
-                     net->b_out, E);
+  hipLaunchKernelGGL(layer1_kernel, stream_grid(nw), dim3(256), 0, s, nw, w, z, net->b[0], t1);
+  if (!gemm_fwd(net->W[1], w, t1)) return DPC_EHIP;
+  hipLaunchKernelGGL(layer2_kernel, stream_grid(nw), dim3(256), 0, s, nw, w, z, net->b[1], t1, t2, h2);
+  if (!gemm_fwd(net->W[2], w, h2)) return DPC_EHIP;
+  // h_3 is used only by the energy: it is never stored; dz_3 replaces z_3
+  hipLaunchKernelGGL(layer3_energy_kernel, dim3((nloc + 3) / 4), dim3(256), 0, s, nloc, w, z, net->b[2],
+                     h2, net->w_out, net->b_out, E, dE_dD ? z : nullptr);
   if (dE_dD) {
-    hipLaunchKernelGGL(delta_init_kernel, stream_grid(nw), dim3(256), 0, s, (int64_t)nloc, w, net->w_out,
-                       delta);
-    for (int l = 2; l >= 1; --l) {   // delta_{l-1} = delta_l + W_l dz_l
-      hipLaunchKernelGGL(tanh_grad_kernel, stream_grid(nw), dim3(256), 0, s, nw, t[l], delta, z);
-      if (rocblas_dgemm(hb, rocblas_operation_transpose, rocblas_operation_none, w, nloc, w, &one,
-                        net->W[l], w, z, w, &one, delta, w) != rocblas_status_success)
-        return DPC_EHIP;
-    }
-    hipLaunchKernelGGL(tanh_grad_kernel, stream_grid(nw), dim3(256), 0, s, nw, t[0], delta, z);
-    if (rocblas_dgemm(hb, rocblas_operation_transpose, rocblas_operation_none, nin, nloc, w, &one,
-                      net->W[0], w, z, w, &zero, dE_dD, nin) != rocblas_status_success)
-      return DPC_EHIP;
+    // delta_2 = w_out + W_3 dz_3; e holds delta - w_out so that the constant
+    // delta_3 = w_out is never stored
+    if (!gemm_bwd(net->W[2], w, &zero, e)) return DPC_EHIP;
+    hipLaunchKernelGGL(tanh_grad_kernel, stream_grid(nw), dim3(256), 0, s, nw, w, t2, net->w_out, e, z);
+    if (!gemm_bwd(net->W[1], w, &one, e)) return DPC_EHIP;   // delta_1 - w_out
+    hipLaunchKernelGGL(tanh_grad_kernel, stream_grid(nw), dim3(256), 0, s, nw, w, t1, net->w_out, e, z);
+    if (!gemm_bwd(net->W[0], nin, &zero, dE_dD)) return DPC_EHIP;
   }
   return dpc_internal_launch_status();
 }

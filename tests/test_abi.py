@@ -221,7 +221,8 @@ def test_env_entry_points_validate_before_launch():
 
 def test_fitting_entry_point_validates_before_launch():
     fake = 4096
-    assert P.dpc_fitting_workspace_bytes(10, 240) == 6 * 10 * 240 * 8
+    assert P.dpc_fitting_workspace_bytes(10, 240) == 5 * 10 * 240 * 8
+    assert P.dpc_fitting_workspace_bytes(5, 7) == 5 * 36 * 8
     assert P.dpc_fitting_workspace_bytes(-1, 240) == 0
     net = P.dpc_fitting_net()
     net.n_in, net.width = 16, 8
