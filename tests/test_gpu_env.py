@@ -217,3 +217,55 @@ def test_chain_positions_to_forces(key):
     err = _normwise(F.cpu().numpy(), Fr)
     print(f"[gpu-env] {c.name} chain forces normwise {err:.2e}", flush=True)
     assert err <= 1e-10
+
+
+@pytest.mark.parametrize("key", ["tiny_water", "cu256"])
+def test_chain_energies_and_forces(key):
+    # GPU: env matrix -> forward -> fitting net -> descriptor backward ->
+    # backward -> forces, against the oracle's same chain (float64)
+    import paper_2107_02103_amd as P
+    import oracle.fitting as fn
+    from oracle.se_a import backward, descriptor_backward, forward
+    from oracle.table import build_tables
+    from synth.system import random_fitting_net
+    x = _inputs(key)
+    c = x.cfg
+    mean, sigma, sigma_all = _stats(x)
+    n = len(x.atype)
+    net = random_fitting_net(np.random.default_rng([2107_02103, 99, 2]), c.m1 * c.m2, (240,) * 3)
+    keep = [torch.from_numpy(np.ascontiguousarray(a)).cuda() for a in net["W"] + net["b"] + [net["w_out"]]]
+    fnet = P.dpc_fitting_net()
+    fnet.n_in, fnet.width, fnet.b_out = c.m1 * c.m2, 240, net["b_out"]
+    for l in range(3):
+        fnet.W[l] = keep[l].data_ptr()
+        fnet.b[l] = keep[3 + l].data_ptr()
+    fnet.w_out = keep[6].data_ptr()
+    op = P.SeATab(x.nets, x.lo, x.L1, x.L2, c.d1, c.d2, c.sel, c.m2)
+    coord, at, nl = _dev(x)
+    s = torch.cuda.current_stream()
+    em = torch.empty((n, c.nnei, 4), dtype=torch.float64, device="cuda")
+    P.dpc_env_mat_a(s, P.DPC_F64, n, c.ntypes, c.nnei, c.box, c.rc, c.rcs, mean, sigma, sigma_all,
+                    coord, at, nl, em)
+    T, D = op.forward(em, nl, at)
+    nb = P.dpc_fitting_workspace_bytes(n, 240)
+    ws = torch.empty(nb // 8, dtype=torch.float64, device="cuda")
+    E = torch.empty(n, dtype=torch.float64, device="cuda")
+    dD = torch.empty_like(D)
+    h = P.RocblasHandle()
+    P.dpc_fitting_fwd_bwd(s, h.value, n, fnet, D, ws, nb, E, dD)
+    dR = op.backward(em, nl, at, op.descriptor_backward(T, dD))
+    F = torch.empty((n, 3), dtype=torch.float64, device="cuda")
+    P.dpc_force_a(s, P.DPC_F64, n, c.ntypes, c.nnei, c.box, c.rc, c.rcs, sigma, sigma_all, coord, at, nl,
+                  _reverse_gpu(x), dR, F, None)
+    torch.cuda.synchronize()
+    h.close()
+    tabs = build_tables(x)
+    emr = ev.env_mat(x.coords, c.box, x.atype, x.nlist, c.rc, c.rcs, mean, sigma, sigma_all)
+    Tr, Dr = forward(emr, x.nlist, x.atype, tabs, c.sel, c.m2)
+    Er, _ = fn.forward(Dr, net)
+    dRr = backward(emr, x.nlist, x.atype, tabs, c.sel, descriptor_backward(Tr, fn.backward(Dr, net)))
+    Fr, _ = ev.force_virial(x.coords, c.box, x.atype, x.nlist, c.rc, c.rcs, mean, sigma, sigma_all, dRr)
+    eE = np.max(np.abs(E.cpu().numpy() - Er)) / np.max(np.abs(Er))
+    eF = _normwise(F.cpu().numpy(), Fr)
+    print(f"[gpu-env] {c.name} chain with fitting net: E {eE:.2e} forces normwise {eF:.2e}", flush=True)
+    assert eE <= 1e-12 and eF <= 1e-10

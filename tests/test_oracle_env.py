@@ -152,3 +152,32 @@ def test_chain_positions_to_forces(tiny_inputs):
             cp[i, a] += h; cm[i, a] -= h
             fd = -(energy(cp, W)[0] - energy(cm, W)[0]) / (2 * h)
             assert abs(fd - F[i, a]) <= 1e-5 * np.max(np.abs(F[i])), (i, a, fd, F[i, a])
+
+
+def test_chain_with_fitting_net(tiny_inputs):
+    # E = sum_i E_i(D_i(r)) through the fitting net: forces from the oracle's
+    # chain against central differences of E in the positions
+    import oracle.fitting as fn
+    from oracle.se_a import backward, descriptor_backward, forward
+    from oracle.table import build_tables
+    from synth.system import random_fitting_net
+    x = tiny_inputs["tiny_water"]
+    c = x.cfg
+    tabs = build_tables(x)
+    mean, sigma, sigma_all = _stats(x)
+    net = random_fitting_net(np.random.default_rng(8), c.m1 * c.m2, (12, 12, 12))
+
+    def energy(coords):
+        em = ev.env_mat(coords, c.box, x.atype, x.nlist, c.rc, c.rcs, mean, sigma, sigma_all)
+        T, D = forward(em, x.nlist, x.atype, tabs, c.sel, c.m2)
+        return float(np.sum(fn.forward(D, net)[0])), em, T, D
+    _, em, T, D = energy(x.coords)
+    dR = backward(em, x.nlist, x.atype, tabs, c.sel, descriptor_backward(T, fn.backward(D, net)))
+    F, _ = ev.force_virial(x.coords, c.box, x.atype, x.nlist, c.rc, c.rcs, mean, sigma, sigma_all, dR)
+    h = 1e-6
+    for i in (1, 6):
+        for a in range(3):
+            cp = x.coords.copy(); cm = x.coords.copy()
+            cp[i, a] += h; cm[i, a] -= h
+            fd = -(energy(cp)[0] - energy(cm)[0]) / (2 * h)
+            assert abs(fd - F[i, a]) <= 1e-5 * np.max(np.abs(F[i])), (i, a, fd, F[i, a])

@@ -74,3 +74,22 @@ def test_single_hidden_layer_closed_form():
     np.testing.assert_allclose(E, t @ net["w_out"] + net["b_out"], rtol=1e-14)
     g = fn.backward(D, net).reshape(len(D), -1)
     np.testing.assert_allclose(g, ((1 - t ** 2) * net["w_out"]) @ net["W"][0].T, rtol=1e-13, atol=1e-15)
+
+
+def test_residual_layers_closed_form():
+    # W_2 = W_3 = 0 with nonzero biases: each residual layer adds the constant
+    # tanh(b_l), so h_3 = h_1 + tanh(b_2) + tanh(b_3), and the gradient is that
+    # of the first layer alone (the constant terms carry none)
+    D, net = _case(3)
+    for l in (1, 2):
+        net["W"][l][:] = 0.0
+    x = D.reshape(len(D), -1)
+    t = np.tanh(x @ net["W"][0] + net["b"][0])
+    h3 = t + np.tanh(net["b"][1]) + np.tanh(net["b"][2])
+    E, _ = fn.forward(D, net)
+    np.testing.assert_allclose(E, h3 @ net["w_out"] + net["b_out"], rtol=1e-14)
+    g = fn.backward(D, net).reshape(len(D), -1)
+    np.testing.assert_allclose(g, ((1 - t ** 2) * net["w_out"]) @ net["W"][0].T, rtol=1e-13, atol=1e-15)
+    # a forward pass without the residual additions misses the first two terms
+    h_plain = np.tanh(np.tanh(t @ net["W"][1] + net["b"][1]) @ net["W"][2] + net["b"][2])
+    assert np.max(np.abs(h_plain @ net["w_out"] + net["b_out"] - E)) > 1e-2
