@@ -395,6 +395,9 @@ def main():
                     help="time the environment matrix and the force / virial assembly instead")
     ap.add_argument("--descriptor-bwd", action="store_true",
                     help="time the descriptor backward (dE/dT from dE/dD) instead of the se_a step")
+    ap.add_argument("--shard", type=int, default=1,
+                    help="time one GPU's share when the workload is split by contiguous atom ranges "
+                         "over this many GPUs: atoms 0 .. natoms/K - 1 (the kernels need no exchange)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (3 times), the known-size "
                          "kernel that calibrates the HBM byte counters, and exit")
@@ -439,13 +442,18 @@ def main():
     log(f"[bench] generating {cfg.name} ({cfg.natoms} atoms, sel {cfg.sel})")
     x = make_inputs(cfg)
     atoms, pairs = cfg.natoms, x.n_valid
+    if args.shard > 1:
+        # the table and the neighbour lists stay those of the whole system;
+        # this GPU's atoms are a contiguous range of rows
+        atoms = cfg.natoms // args.shard
+        pairs = int(np.count_nonzero(x.nlist[:atoms] >= 0))
     log(f"[bench] inputs ready in {time.perf_counter() - t:.1f} s: {pairs} valid pairs")
 
     op = P.SeATab(x.nets, x.lo, x.L1, x.L2, cfg.d1, cfg.d2, cfg.sel, cfg.m2, dtype=mode)
-    em = torch.from_numpy(x.em.astype(store, copy=False)).cuda()
-    nl = torch.from_numpy(x.nlist).cuda()
-    at = torch.from_numpy(x.atype).cuda()
-    dT = torch.from_numpy(x.dT.astype(store, copy=False)).cuda()
+    em = torch.from_numpy(x.em[:atoms].astype(store, copy=False)).cuda()
+    nl = torch.from_numpy(x.nlist[:atoms]).cuda()
+    at = torch.from_numpy(x.atype[:atoms]).cuda()
+    dT = torch.from_numpy(x.dT[:atoms].astype(store, copy=False)).cuda()
     tacc = torch.float32 if dtype == "f32" else torch.float64
     T = torch.empty((atoms, cfg.m1, 4), dtype=tacc, device="cuda")
     D = torch.empty((atoms, cfg.m1, cfg.m2), dtype=tacc, device="cuda")
@@ -504,7 +512,8 @@ def main():
         "config": {"workload": f"{cfg.name}: {cfg.kind} {cfg.ncell}^3 cells, {atoms} atoms, "
                                f"rc {cfg.rc}, rcs {cfg.rcs}, sel {list(cfg.sel)}, "
                                f"embedding {'-'.join(map(str, cfg.widths))}, M2 {cfg.m2}, "
-                               f"table stride {cfg.d1}/{cfg.d2}",
+                               f"table stride {cfg.d1}/{cfg.d2}"
+                               + (f"; one GPU's share of {args.shard}: atoms 0..{atoms - 1}" if args.shard > 1 else ""),
                    "atoms": atoms, "valid_pairs": pairs, "nnei": cfg.nnei,
                    "table_bytes": int(op.coeff.numel() * op.coeff.element_size())},
         "tflops_algorithmic": tflops,
@@ -513,7 +522,7 @@ def main():
         "bwd_ms": bwd_ms,
         "roofline": {"bound": bound, "kernel": dom, "achieved": achieved, "peak": peak,
                      "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": None if args.stride else hbm_traffic(cfg.name, dom)},
+                     "traffic": None if (args.stride or args.shard > 1) else hbm_traffic(cfg.name, dom)},
     }
     del T, D, dR, em, dT
     torch.cuda.empty_cache()

@@ -244,8 +244,9 @@ size_t dpc_fitting_workspace_bytes(int nloc, int width);
  * D [nloc][n_in] (float64, device).  The layer products run as rocBLAS
  * double-precision GEMMs on the caller's handle `blas` (a rocblas_handle as
  * void*; its stream is set to `stream`, and its pointer mode must be host);
- * the library allocates nothing: `workspace` (device, 16-byte aligned,
- * >= dpc_fitting_workspace_bytes) is the caller's.  Sums have a fixed order
+ * this library allocates nothing: `workspace` (device, 16-byte aligned,
+ * >= dpc_fitting_workspace_bytes) is the caller's (rocBLAS may keep a
+ * workspace of its own inside the handle).  Sums have a fixed order
  * for a given rocBLAS.  DPC_EHIP reports a HIP or rocBLAS failure.          */
 int dpc_fitting_fwd_bwd(void* stream, void* blas, int nloc, const dpc_fitting_net* net,
                         const double* D, void* workspace, size_t workspace_bytes, double* E,
