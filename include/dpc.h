@@ -243,7 +243,8 @@ size_t dpc_fitting_workspace_bytes(int nloc, int width);
 /* E [nloc] and, if dE_dD is not NULL, dE/dD [nloc][n_in] (float64) for
  * D [nloc][n_in] (float64, device).  The layer products run as rocBLAS
  * double-precision GEMMs on the caller's handle `blas` (a rocblas_handle as
- * void*; its stream is set to `stream`, and its pointer mode must be host);
+ * void*; its stream is left set to `stream`; its pointer mode is host for
+ * the call and restored after it);
  * this library allocates nothing: `workspace` (device, 16-byte aligned,
  * >= dpc_fitting_workspace_bytes) is the caller's (rocBLAS may keep a
  * workspace of its own inside the handle).  Sums have a fixed order

@@ -289,7 +289,8 @@ def dpc_fitting_fwd_bwd(stream, blas, nloc, net, D, workspace, workspace_bytes, 
 
 class RocblasHandle:
     """A rocBLAS handle for dpc_fitting_fwd_bwd, created and destroyed through
-    librocblas (the caller owns it; the library only sets its stream)."""
+    librocblas (the caller owns it; the library leaves its stream set to the
+    call's and restores its pointer mode)."""
 
     def __init__(self):
         self._rb = C.CDLL("librocblas.so.5")
@@ -299,6 +300,19 @@ class RocblasHandle:
         if self._rb.rocblas_create_handle(C.byref(h)) != 0:
             raise RuntimeError("rocblas_create_handle failed")
         self.value = h.value
+
+    def pointer_mode(self):
+        """0 = host, 1 = device (rocblas_pointer_mode)."""
+        m = C.c_int()
+        self._rb.rocblas_get_pointer_mode.argtypes = [C.c_void_p, C.POINTER(C.c_int)]
+        if self._rb.rocblas_get_pointer_mode(C.c_void_p(self.value), C.byref(m)) != 0:
+            raise RuntimeError("rocblas_get_pointer_mode failed")
+        return m.value
+
+    def set_pointer_mode(self, mode):
+        self._rb.rocblas_set_pointer_mode.argtypes = [C.c_void_p, C.c_int]
+        if self._rb.rocblas_set_pointer_mode(C.c_void_p(self.value), int(mode)) != 0:
+            raise RuntimeError("rocblas_set_pointer_mode failed")
 
     def close(self):
         if self.value:

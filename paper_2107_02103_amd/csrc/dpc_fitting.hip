@@ -158,6 +158,20 @@ extern "C" int dpc_fitting_fwd_bwd(void* stream, void* blas, int nloc, const dpc
   hipStream_t s = static_cast<hipStream_t>(stream);
   rocblas_handle hb = static_cast<rocblas_handle>(blas);
   if (rocblas_set_stream(hb, s) != rocblas_status_success) return DPC_EHIP;
+  // alpha and beta live on the host: host pointer mode for this call, the
+  // caller's mode restored on every return
+  struct ModeGuard {
+    rocblas_handle h;
+    rocblas_pointer_mode old = rocblas_pointer_mode_host;
+    bool set = false;
+    ~ModeGuard() {
+      if (set) rocblas_set_pointer_mode(h, old);
+    }
+  } mode{hb};
+  if (rocblas_get_pointer_mode(hb, &mode.old) != rocblas_status_success ||
+      rocblas_set_pointer_mode(hb, rocblas_pointer_mode_host) != rocblas_status_success)
+    return DPC_EHIP;
+  mode.set = true;
   const int64_t nw = (int64_t)nloc * w;
   double* ws = static_cast<double*>(workspace);
   const int64_t np = nw + (nw & 1);   // array pitch: keeps every array 16-byte aligned

@@ -10,7 +10,7 @@ torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
 
-def _run(n, m1, m2, width, seed, sample=None):
+def _run(n, m1, m2, width, seed, sample=None, device_mode=False):
     import paper_2107_02103_amd as P
     rng = np.random.default_rng([2107_02103, 66, seed])
     net = random_fitting_net(rng, m1 * m2, (width,) * 3)
@@ -29,8 +29,11 @@ def _run(n, m1, m2, width, seed, sample=None):
     E = torch.full((n,), float("nan"), dtype=torch.float64, device="cuda")
     G = torch.full((n, m1, m2), float("nan"), dtype=torch.float64, device="cuda")
     h = P.RocblasHandle()
+    if device_mode:
+        h.set_pointer_mode(1)
     P.dpc_fitting_fwd_bwd(torch.cuda.current_stream(), h.value, n, c, Dg, ws, nb, E, G)
     torch.cuda.synchronize()
+    assert h.pointer_mode() == (1 if device_mode else 0)   # the caller's mode is restored
     h.close()
     atoms = np.arange(n) if sample is None else sample
     Er, _ = fn.forward(D[atoms], net)
@@ -47,6 +50,13 @@ def _run(n, m1, m2, width, seed, sample=None):
 @pytest.mark.parametrize("n,m1,m2,width", [(37, 100, 16, 240), (5, 3, 2, 7), (1, 1, 1, 1), (300, 20, 4, 33)])
 def test_parity(n, m1, m2, width):
     eE, eG = _run(n, m1, m2, width, seed=n + width)
+    assert eE <= 1e-12 and eG <= 1e-12
+
+
+def test_caller_handle_in_device_pointer_mode():
+    # the entry point passes alpha and beta from the host whatever the
+    # handle's mode, and gives the handle back in the caller's mode
+    eE, eG = _run(19, 10, 4, 24, seed=5, device_mode=True)
     assert eE <= 1e-12 and eG <= 1e-12
 
 
