@@ -66,7 +66,8 @@ __device__ __forceinline__ void weight(const EnvGeo& g, double r, double& s, dou
 
 // workgroup b covers slots 256 c .. 256 c + 255 of atom b / chunks (c = b mod
 // chunks), so that the atom index is uniform; rows are written 16 bytes at a
-// time when the output is 16-byte aligned (kPair)
+// time when the output is 16-byte aligned (kPair), float64 rows of whole
+// wavefronts in contiguous 1 KB stores
 template <typename TO, bool kPair>
 __global__ __launch_bounds__(256) void env_mat_kernel(const EnvGeo g, int chunks,
                                                       const double* __restrict__ coord,
@@ -97,6 +98,23 @@ __global__ __launch_bounds__(256) void env_mat_kernel(const EnvGeo g, int chunks
   TO* o = em + 4 * e;
   if constexpr (kPair && sizeof(TO) == 8) {
     typedef double D2 __attribute__((ext_vector_type(2)));
+    // a wavefront whose 64 slots are all in the list writes its 2 KB of rows
+    // as two fully contiguous 1 KB stores, transposed through LDS (each lane
+    // storing its own 32-byte row leaves every store instruction with gaps)
+    __shared__ __align__(16) D2 stage[4][128];
+    const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+    const int sw = __builtin_amdgcn_readfirstlane(s - l);
+    if (sw + 64 <= g.nnei) {
+      stage[w][2 * l] = D2{row[0], row[1]};
+      stage[w][2 * l + 1] = D2{row[2], row[3]};
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      D2* ow = reinterpret_cast<D2*>(em + 4 * ((size_t)i * g.nnei + sw));
+      __builtin_nontemporal_store(stage[w][l], ow + l);
+      __builtin_nontemporal_store(stage[w][l + 64], ow + l + 64);
+      return;
+    }
     __builtin_nontemporal_store(D2{row[0], row[1]}, reinterpret_cast<D2*>(o));
     __builtin_nontemporal_store(D2{row[2], row[3]}, reinterpret_cast<D2*>(o) + 1);
   } else if constexpr (kPair) {
