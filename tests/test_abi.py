@@ -247,3 +247,16 @@ def test_fitting_entry_point_validates_before_launch():
     assert e.value.status == B.DPC_EINVAL
     net.W[1] = fake
     P.dpc_fitting_fwd_bwd(0, 0, 0, net, 0, 0, 0, 0)                   # nloc = 0: no-op
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    # the product path has no fallback: without the built library the first
+    # use of any entry point raises ImportError
+    import subprocess
+    import sys
+    code = "import paper_2107_02103_amd as P; P.dpc_version()"
+    env = dict(os.environ, DPC_LIBRARY=str(tmp_path / "absent" / "libdpc.so"))
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True, text=True,
+                       timeout=300)
+    assert r.returncode != 0
+    assert "ImportError" in r.stderr and "libdpc.so not found" in r.stderr
