@@ -79,4 +79,4 @@ def test_deterministic_and_thread_independent():
 def test_config_shapes():
     assert [c.natoms for c in CONFIGS] == [256, 12288, 32000, 1048576, 331776]
     assert [c.nnei for c in CONFIGS] == [128, 138, 420, 512, 138]
-    assert abs(CONFIGS[1].box - 49.669) < 1e-3 and abs(CONFIGS[4].box - 149.0) < 0.01
+    assert abs(get_config("water4096").box - 49.669) < 1e-3 and abs(get_config("water110592").box - 149.0) < 0.01
