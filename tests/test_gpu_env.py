@@ -219,7 +219,7 @@ def test_chain_positions_to_forces(key):
     assert err <= 1e-10
 
 
-@pytest.mark.parametrize("key", ["tiny_water", "cu256"])
+@pytest.mark.parametrize("key", ["tiny_water", "tiny_alloy", "cu256"])
 def test_chain_energies_and_forces(key):
     # GPU: env matrix -> forward -> fitting net -> descriptor backward ->
     # backward -> forces, against the oracle's same chain (float64)
