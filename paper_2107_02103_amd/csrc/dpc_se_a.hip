@@ -524,6 +524,11 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_fwd_kernel(
     }
   }
   TI cfA[6][CPL], cfB[6][CPL];
+  // lanes without channels (lane * CPL >= m1) load coefficients like the
+  // others, so that every load stays unconditional, but skip the arithmetic:
+  // idle float64 FMAs still draw power, and this kernel runs at a lower
+  // clock than the rest
+  const bool active = lane * CPL < m1;
 
   // Chunk sets are visited cyclically from a start that differs between
   // wavefronts, so that waves sharing a SIMD are not all building (a
@@ -565,6 +570,7 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_fwd_kernel(
           for (int k = 0; k < 4; ++k) ac[h][k] = fma((TA)v, (TA)c.r[k], ac[h][k]);
         }
       };
+      if (!active) return;
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
         const int lo = b == 0 ? S : split_at<NB>(p, b);
