@@ -203,6 +203,22 @@ def _sel(sel):
     return (C.c_int * len(sel))(*[int(s) for s in sel])
 
 
+def _need(x, count, esize, name):
+    """A tensor argument must hold at least `count` elements of `esize`
+    bytes: the library cannot see the size of a device buffer, so an
+    undersized one is refused here, before anything is launched."""
+    if x is None or isinstance(x, int):
+        return
+    have = x.numel() * x.element_size()
+    if have < int(count) * esize:
+        raise ValueError(f"{name} holds {have} bytes, needs {int(count) * esize}")
+
+
+def _io_sizes(dtype):
+    """(input element bytes, output element bytes) of a dtype mode."""
+    return {DPC_F64: (8, 8), DPC_F32: (4, 4), DPC_F32_ACC64: (4, 8)}.get(int(dtype), (8, 8))
+
+
 def _stream(stream):
     if stream is None:
         return None
@@ -213,6 +229,9 @@ def _stream(stream):
 
 def dpc_se_a_tab_fwd(stream, dtype, nloc, ntypes, sel, m1, m2, ranges, coeff, atype, nlist, em,
                      T, D):
+    nnei, (ei, eo) = sum(int(v) for v in sel), _io_sizes(dtype)
+    _need(atype, nloc, 4, "atype"); _need(nlist, nloc * nnei, 4, "nlist")
+    _need(em, nloc * nnei * 4, ei, "em"); _need(T, nloc * m1 * 4, eo, "T"); _need(D, nloc * m1 * m2, eo, "D")
     _check(_lib.dpc_se_a_tab_fwd(_stream(stream), int(dtype), int(nloc), int(ntypes), _sel(sel),
                                  int(m1), int(m2), ranges, _ptr(coeff, name="coeff"),
                                  _ptr(atype, name="atype"), _ptr(nlist, name="nlist"),
@@ -222,6 +241,10 @@ def dpc_se_a_tab_fwd(stream, dtype, nloc, ntypes, sel, m1, m2, ranges, coeff, at
 
 def dpc_se_a_tab_bwd(stream, dtype, nloc, ntypes, sel, m1, ranges, coeff, atype, nlist, em,
                      dE_dT, dE_dem):
+    nnei, (ei, eo) = sum(int(v) for v in sel), _io_sizes(dtype)
+    _need(atype, nloc, 4, "atype"); _need(nlist, nloc * nnei, 4, "nlist")
+    _need(em, nloc * nnei * 4, ei, "em"); _need(dE_dT, nloc * m1 * 4, ei, "dE_dT")
+    _need(dE_dem, nloc * nnei * 4, eo, "dE_dem")
     _check(_lib.dpc_se_a_tab_bwd(_stream(stream), int(dtype), int(nloc), int(ntypes), _sel(sel),
                                  int(m1), ranges, _ptr(coeff, name="coeff"),
                                  _ptr(atype, name="atype"), _ptr(nlist, name="nlist"),
@@ -231,6 +254,10 @@ def dpc_se_a_tab_bwd(stream, dtype, nloc, ntypes, sel, m1, ranges, coeff, atype,
 
 
 def dpc_descriptor_bwd(stream, dtype, nloc, m1, m2, T, dE_dD, dE_dT):
+    ei = 4 if int(dtype) == DPC_F32 else 8
+    eo = 8 if int(dtype) == DPC_F64 else 4
+    _need(T, nloc * m1 * 4, ei, "T"); _need(dE_dD, nloc * m1 * m2, ei, "dE_dD")
+    _need(dE_dT, nloc * m1 * 4, eo, "dE_dT")
     _check(_lib.dpc_descriptor_bwd(_stream(stream), int(dtype), int(nloc), int(m1), int(m2),
                                    _ptr(T, name="T"), _ptr(dE_dD, name="dE_dD"),
                                    _ptr(dE_dT, name="dE_dT")),
@@ -249,6 +276,8 @@ def dpc_env_mat_a(stream, dtype, nloc, ntypes, nnei, box, rc, rcs, mean, sigma, 
     pm, km = _dvec(mean, ntypes, "mean")
     ps, ks = _dvec(sigma, ntypes, "sigma")
     pa, ka = _dvec(sigma_all, ntypes, "sigma_all")
+    _need(coord, nloc * 3, 8, "coord"); _need(atype, nloc, 4, "atype")
+    _need(nlist, nloc * nnei, 4, "nlist"); _need(em, nloc * nnei * 4, 8 if int(dtype) == DPC_F64 else 4, "em")
     _check(_lib.dpc_env_mat_a(_stream(stream), int(dtype), int(nloc), int(ntypes), int(nnei),
                               float(box), float(rc), float(rcs), pm, ps, pa, _ptr(coord, name="coord"),
                               _ptr(atype, name="atype"), _ptr(nlist, name="nlist"), _ptr(em, name="em")),
@@ -256,6 +285,9 @@ def dpc_env_mat_a(stream, dtype, nloc, ntypes, nnei, box, rc, rcs, mean, sigma, 
 
 
 def dpc_nlist_reverse(stream, nloc, ntypes, sel, box, coord, atype, nlist, rev):
+    nnei = sum(int(v) for v in sel)
+    _need(coord, nloc * 3, 8, "coord"); _need(atype, nloc, 4, "atype")
+    _need(nlist, nloc * nnei, 4, "nlist"); _need(rev, nloc * nnei, 4, "rev")
     _check(_lib.dpc_nlist_reverse(_stream(stream), int(nloc), int(ntypes), _sel(sel), float(box),
                                   _ptr(coord, name="coord"), _ptr(atype, name="atype"),
                                   _ptr(nlist, name="nlist"), _ptr(rev, name="rev")),
@@ -266,6 +298,10 @@ def dpc_force_a(stream, dtype, nloc, ntypes, nnei, box, rc, rcs, sigma, sigma_al
                 nlist, rev, dE_dem, force, virial=None):
     ps, ks = _dvec(sigma, ntypes, "sigma")
     pa, ka = _dvec(sigma_all, ntypes, "sigma_all")
+    _need(coord, nloc * 3, 8, "coord"); _need(atype, nloc, 4, "atype")
+    _need(nlist, nloc * nnei, 4, "nlist"); _need(rev, nloc * nnei, 4, "rev")
+    _need(dE_dem, nloc * nnei * 4, 4 if int(dtype) == DPC_F32 else 8, "dE_dem")
+    _need(force, nloc * 3, 8, "force"); _need(virial, nloc * 9, 8, "virial")
     _check(_lib.dpc_force_a(_stream(stream), int(dtype), int(nloc), int(ntypes), int(nnei),
                             float(box), float(rc), float(rcs), ps, pa, _ptr(coord, name="coord"),
                             _ptr(atype, name="atype"), _ptr(nlist, name="nlist"),
@@ -281,6 +317,8 @@ def dpc_fitting_workspace_bytes(nloc, width):
 def dpc_fitting_fwd_bwd(stream, blas, nloc, net, D, workspace, workspace_bytes, E, dE_dD=None):
     """``net``: a dpc_fitting_net whose pointers are device addresses;
     ``blas``: a rocblas_handle (int), see RocblasHandle."""
+    _need(D, nloc * net.n_in, 8, "D"); _need(E, nloc, 8, "E"); _need(dE_dD, nloc * net.n_in, 8, "dE_dD")
+    _need(workspace, workspace_bytes, 1, "workspace")
     _check(_lib.dpc_fitting_fwd_bwd(_stream(stream), blas, int(nloc), C.byref(net), _ptr(D, name="D"),
                                     _ptr(workspace, name="workspace"), int(workspace_bytes),
                                     _ptr(E, name="E"), _ptr(dE_dD, name="dE_dD")),

@@ -260,3 +260,29 @@ def test_missing_library_fails_loudly(tmp_path):
                        timeout=300)
     assert r.returncode != 0
     assert "ImportError" in r.stderr and "libdpc.so not found" in r.stderr
+
+
+def test_binding_refuses_undersized_tensors():
+    # device buffers carry no size through the C ABI: the binding checks the
+    # tensors it is given before the call (CPU tensors suffice here)
+    torch = pytest.importorskip("torch")
+    f64 = lambda n: torch.zeros(n, dtype=torch.float64)
+    i32 = lambda n: torch.zeros(n, dtype=torch.int32)
+    with pytest.raises(ValueError, match="dE_dT"):
+        P.dpc_descriptor_bwd(0, P.DPC_F64, 3, 8, 4, f64(3 * 8 * 4), f64(3 * 8 * 4), f64(3 * 8 * 4 - 1))
+    with pytest.raises(ValueError, match="em"):
+        P.dpc_env_mat_a(0, P.DPC_F64, 2, 1, 5, 20.0, 6.0, 0.5, [0.0], [1.0], [1.0], f64(6), i32(2), i32(10),
+                        f64(2 * 5 * 4 - 1))
+    with pytest.raises(ValueError, match="rev"):
+        P.dpc_nlist_reverse(0, 2, 1, [5], 20.0, f64(6), i32(2), i32(10), i32(9))
+    with pytest.raises(ValueError, match="virial"):
+        P.dpc_force_a(0, P.DPC_F64, 2, 1, 5, 20.0, 6.0, 0.5, [1.0], [1.0], f64(6), i32(2), i32(10), i32(10),
+                      f64(40), f64(6), f64(17))
+    net = P.dpc_fitting_net()
+    net.n_in, net.width = 16, 8
+    with pytest.raises(ValueError, match="D"):
+        P.dpc_fitting_fwd_bwd(0, 1, 4, net, f64(63), f64(1000), 8000, f64(4))
+    with pytest.raises(ValueError, match="workspace"):
+        P.dpc_fitting_fwd_bwd(0, 1, 4, net, f64(64), f64(99), 800, f64(4))
+    with pytest.raises(ValueError, match="nlist"):
+        P.dpc_se_a_tab_fwd(0, P.DPC_F64, 2, 1, [5], 8, 4, None, 0, i32(2), i32(9), f64(40), f64(64), f64(64))
