@@ -66,3 +66,38 @@ def test_parity_full_size_cu1m_sampled():
     sample = np.unique(np.concatenate([np.random.default_rng(3).choice(n, 48, replace=False), [0, n - 1]]))
     eE, eG = _run(n, 100, 16, 240, seed=7, sample=sample)
     assert eE <= 1e-12 and eG <= 1e-12
+
+
+def test_saturated_and_nan_inputs():
+    # descriptors scaled by 50 drive |z| far past 20 (tanh rounds to +-1
+    # there); a NaN descriptor stays in its own atom's energy and gradient
+    import paper_2107_02103_amd as P
+    n, m1, m2, width = 9, 10, 4, 24
+    rng = np.random.default_rng([2107_02103, 66, 99])
+    net = random_fitting_net(rng, m1 * m2, (width,) * 3)
+    D = 50.0 * random_grad(rng, n, m1, width=m2)
+    D[4, 3, 1] = np.nan
+    dev = [torch.from_numpy(np.ascontiguousarray(a)).cuda() for a in net["W"] + net["b"] + [net["w_out"]]]
+    c = P.dpc_fitting_net()
+    c.n_in, c.width, c.b_out = m1 * m2, width, net["b_out"]
+    for l in range(3):
+        c.W[l] = dev[l].data_ptr()
+        c.b[l] = dev[3 + l].data_ptr()
+    c.w_out = dev[6].data_ptr()
+    nb = P.dpc_fitting_workspace_bytes(n, width)
+    ws = torch.empty(nb // 8, dtype=torch.float64, device="cuda")
+    E = torch.empty(n, dtype=torch.float64, device="cuda")
+    G = torch.empty((n, m1, m2), dtype=torch.float64, device="cuda")
+    h = P.RocblasHandle()
+    P.dpc_fitting_fwd_bwd(torch.cuda.current_stream(), h.value, n, c, torch.from_numpy(D).cuda(), ws, nb, E, G)
+    torch.cuda.synchronize()
+    h.close()
+    E, G = E.cpu().numpy(), G.cpu().numpy()
+    ok = np.arange(n) != 4
+    assert np.isnan(E[4]) and np.all(np.isnan(G[4]))
+    Er, _ = fn.forward(D[ok], net)
+    Gr = fn.backward(D[ok], net)
+    eE = np.max(np.abs(E[ok] - Er)) / np.max(np.abs(Er))
+    eG = max(np.max(np.abs(G[ok][a] - Gr[a])) / max(np.max(np.abs(Gr[a])), 1e-300) for a in range(len(Gr)))
+    print(f"[gpu-fitting] saturated inputs: E {eE:.2e} dE/dD {eG:.2e}", flush=True)
+    assert eE <= 1e-12 and eG <= 1e-12
