@@ -17,13 +17,19 @@ _LIB = os.path.join(_HERE, "_build", "libse_a_ref.so")
 _lib = None
 
 
+def compile_source(src, out):
+    """Compile a C oracle source file into the shared library ``out``."""
+    tmp = out + ".tmp%d" % os.getpid()
+    subprocess.check_call(["gcc", "-O2", "-ffp-contract=off", "-fopenmp", "-fPIC",
+                           "-shared", "-std=c11", src, "-o", tmp, "-lm"])
+    os.replace(tmp, out)
+    return out
+
+
 def build(force=True):
     os.makedirs(os.path.dirname(_LIB), exist_ok=True)
     if force or not os.path.exists(_LIB):
-        tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.check_call(["gcc", "-O2", "-ffp-contract=off", "-fopenmp", "-fPIC",
-                               "-shared", "-std=c11", _SRC, "-o", tmp, "-lm"])
-        os.replace(tmp, _LIB)
+        compile_source(_SRC, _LIB)
     return _LIB
 
 
@@ -36,15 +42,22 @@ class _Args(C.Structure):
                 ("nlist", C.c_void_p), ("em", C.c_void_p)]
 
 
+def load_library(path):
+    """ctypes handle of a compiled C oracle (the default one, or a copy built
+    from a modified source by a test)."""
+    lib = C.CDLL(path)
+    for fn in (lib.ref_forward, lib.ref_backward):
+        fn.restype = None
+    lib.ref_num_threads.restype = C.c_int
+    return lib
+
+
 def _load():
     global _lib
     if _lib is None:
         if not os.path.exists(_LIB):
             build(force=False)
-        _lib = C.CDLL(_LIB)
-        for fn in (_lib.ref_forward, _lib.ref_backward):
-            fn.restype = None
-        _lib.ref_num_threads.restype = C.c_int
+        _lib = load_library(_LIB)
     return _lib
 
 
@@ -55,7 +68,8 @@ def num_threads():
 class Problem:
     """Holds contiguous inputs and the flattened tables for the C oracle."""
 
-    def __init__(self, em, nlist, atype, tables, sel, m2):
+    def __init__(self, em, nlist, atype, tables, sel, m2, lib=None):
+        self._lib = lib
         self.em = np.ascontiguousarray(em, np.float64)
         self.nlist = np.ascontiguousarray(nlist, np.int32)
         self.atype = np.ascontiguousarray(atype, np.int32)
@@ -81,7 +95,7 @@ class Problem:
         i1 = self.nlist.shape[0] if i1 is None else i1
         T = np.empty((i1 - i0, self.M, 4))
         D = np.empty((i1 - i0, self.M, self.m2))
-        _load().ref_forward(C.byref(self._args), C.c_int64(i0), C.c_int64(i1),
+        (self._lib or _load()).ref_forward(C.byref(self._args), C.c_int64(i0), C.c_int64(i1),
                             T.ctypes.data_as(C.c_void_p), D.ctypes.data_as(C.c_void_p))
         return T, D
 
@@ -91,6 +105,6 @@ class Problem:
         dT = np.ascontiguousarray(dT, np.float64)
         assert dT.shape == (i1 - i0, self.M, 4)
         dR = np.empty((i1 - i0, self.nlist.shape[1], 4))
-        _load().ref_backward(C.byref(self._args), C.c_int64(i0), C.c_int64(i1),
+        (self._lib or _load()).ref_backward(C.byref(self._args), C.c_int64(i0), C.c_int64(i1),
                              dT.ctypes.data_as(C.c_void_p), dR.ctypes.data_as(C.c_void_p))
         return dR
