@@ -62,6 +62,7 @@ constexpr size_t kMaxLds = 65536;    // LDS a workgroup may take without opting 
 
 struct PairRange {             // one ordered type pair's table, as the kernels see it
   double lo, d1, d2;
+  double x_up, x_end;          // ends of the main range and of the band (formed on the host)
   int L1, L2;
   int offset;                  // element offset of the pair's coefficients
   int pad;
@@ -121,19 +122,22 @@ __device__ __forceinline__ int block_of(const Geo& g, int j) {
 __device__ __forceinline__ int key_offset(int key) { return kOffMask - (key & kOffMask); }
 
 // Interval of x in one pair's table (see dpc_range in dpc.h).  Always float64.
+// The range ends come from the host and the node is rounded on its own (no
+// fused multiply-add), so every x gets the interval and offset that a plain
+// evaluation of the same formulas gives.  NaN takes the clamped branch.
 __device__ __forceinline__ void locate(const PairRange& P, double x, int& l, double& t,
                                        bool& clamped) {
+#pragma clang fp contract(off)
   // one division: origin, stride and last index of the part (main range or
   // band) that x falls in are selected first, so lanes do not diverge
-  const double x_up = P.lo + (double)P.L1 * P.d1;
-  const double x_end = x_up + (double)P.L2 * P.d2;
-  const bool main = x < x_up;
-  const double org = main ? P.lo : x_up, d = main ? P.d1 : P.d2;
+  const bool main = x < P.x_up;
+  const double org = main ? P.lo : P.x_up, d = main ? P.d1 : P.d2;
   double q = floor((x - org) / d);
   q = fmin(fmax(q, 0.0), (double)((main ? P.L1 : P.L2) - 1));
   l = (main ? 0 : P.L1) + (int)q;
-  t = x - (org + q * d);
-  clamped = !(x < x_end);
+  const double node = org + q * d;
+  t = x - node;
+  clamped = !(x < P.x_end);
   if (clamped) {
     l = P.L1 + P.L2 - 1;
     t = P.d2;
@@ -363,7 +367,9 @@ __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[
       locate(P, (double)rec.r[0], l, rec.t, cl);
       rec.pad = 0.0;
       key = (blk << kOffBits) | (kOffMask - (P.offset + l * 6 * g.ld));
-      if (kBwd && cl) {
+      // beyond the table the derivative term vanishes: a zero row removes it
+      // (a NaN or infinite x keeps its row, so that it propagates)
+      if (kBwd && cl && isfinite(rec.r[0])) {
 #pragma unroll
         for (int k = 0; k < 4; ++k) rec.r[k] = (TI)0;
       }
@@ -1075,14 +1081,16 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
     }
   }
 
-  // copy the interval whose coefficients start at element `off` into the slot
+  // copy the interval whose coefficients start at element `off` into the slot;
+  // the interval's offset goes into the range-checked vector offset, so
+  // that the bytes read past the last interval of the buffer come back as 0
   auto fetch = [&](int off) __attribute__((always_inline)) {
-    const int soff = off * (int)sizeof(double);
+    const int voff = off * (int)sizeof(double) + lane * 16;
 #pragma unroll
     for (int i = 0; i < NS; ++i)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rs, (__attribute__((address_space(3))) void*)(slot_p + 1024 * i), 16, lane * 16,
-          soff + 1024 * i, 0, 0);
+          rs, (__attribute__((address_space(3))) void*)(slot_p + 1024 * i), 16, voff + 1024 * i,
+          0, 0, 0);
   };
 
   const int nch = (nnei + kC - 1) / kC;
@@ -1231,6 +1239,7 @@ int launch_status() {
 // Host-side validation shared by both passes; fills the kernel geometry.
 int make_geo(int nloc, int ntypes, const int* sel, int m1, int m2, const dpc_range* ranges,
              size_t elem_bytes, Geo* g) {
+#pragma clang fp contract(off)
   if (nloc < 0 || ntypes < 1 || !sel || !ranges || m1 < 1 || m2 < 1 || m2 > m1)
     return DPC_EINVAL;
   if (ntypes > DPC_MAX_TYPES || m1 > DPC_MAX_M1) return DPC_ENOTSUP;
@@ -1257,6 +1266,8 @@ int make_geo(int nloc, int ntypes, const int* sel, int m1, int m2, const dpc_ran
     q.lo = r.lo;
     q.d1 = r.d1;
     q.d2 = r.d2;
+    q.x_up = r.lo + (double)r.L1 * r.d1;
+    q.x_end = q.x_up + (double)r.L2 * r.d2;
     q.L1 = (int)r.L1;
     q.L2 = (int)r.L2;
     q.offset = (int)r.offset;

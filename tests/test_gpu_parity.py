@@ -77,11 +77,34 @@ def test_parity_f64(key):
     _check(x, _sample(n, 300), got, "f64")
 
 
-@pytest.mark.timeout(600)
+def _all_atoms_normwise(x, out, dtype, chunk=65536):
+    """Every atom's T, D and dE/dR~ normwise against the C oracle, in chunks
+    of atoms (the oracle's tables are built once)."""
+    from oracle import cref
+    from parity import normwise, oracle_view
+    tabs, em, nl, at, dT = oracle_view(x, slice(None), dtype)
+    pb = cref.Problem(em, nl, at, tabs, x.cfg.sel, x.cfg.m2)
+    n = nl.shape[0]
+    worst = {"T": 0.0, "D": 0.0, "dR": 0.0}
+    for a0 in range(0, n, chunk):
+        a1 = min(n, a0 + chunk)
+        T, D = pb.forward(a0, a1)
+        dR = pb.backward(dT[a0:a1], a0, a1)
+        for name, g, r in zip(("T", "D", "dR"), out, (T, D, dR)):
+            worst[name] = max(worst[name], normwise(g[a0:a1].cpu().numpy().astype(np.float64), r))
+        # padding rows of dE/dR~ are exactly zero
+        assert np.all(out[2][a0:a1].cpu().numpy()[nl[a0:a1] < 0] == 0)
+    print(f"[gpu-parity] {x.cfg.name} {dtype} all {n} atoms normwise {worst}", flush=True)
+    assert max(worst.values()) <= TOL[dtype], worst
+
+
+@pytest.mark.timeout(900)
 def test_parity_f64_full_size_cu1m():
-    # the benchmarked workload (1,048,576 atoms, sel 512), sampled outputs
+    # the benchmarked workload (1,048,576 atoms, sel 512): every atom
+    # normwise, a sample componentwise
     x = _inputs(3)
     _, _, out = _run_gpu(x, "f64")
+    _all_atoms_normwise(x, out, "f64")
     atoms = _sample(x.nlist.shape[0], 400, seed=3)
     got = tuple(t[torch.from_numpy(atoms).cuda()].cpu().numpy() for t in out)
     tol = TOL["f64"]
@@ -94,11 +117,14 @@ def test_parity_f64_full_size_cu1m():
     torch.cuda.empty_cache()
 
 
-@pytest.mark.timeout(600)
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("dtype", ["f32", "f32acc64", "f64"])
 def test_parity_water_large_modes(dtype):
+    # water110592 (331,776 atoms) in all three modes: every atom normwise, a
+    # sample componentwise
     x = _inputs(4)
     _, _, out = _run_gpu(x, dtype)
+    _all_atoms_normwise(x, out, dtype)
     atoms = _sample(x.nlist.shape[0], 300, seed=4)
     got = tuple(t[torch.from_numpy(atoms).cuda()].cpu().numpy().astype(np.float64) for t in out)
     tol = TOL[dtype]
@@ -124,34 +150,11 @@ def test_deterministic_bitwise():
     assert torch.equal(out1[0], T2) and torch.equal(out1[1], D2) and torch.equal(out1[2], dR2)
 
 
-def _synthetic(nloc, sel, m1, m2, seed, lo=-0.6, L1=300, L2=30, d1=0.01, d2=0.1):
-    """Inputs with hand-placed neighbours for edge cases (oracle-ready)."""
-    from synth.system import Inputs, random_net
-    from synth.configs import Config
-    rng = np.random.default_rng(seed)
-    nt = len(sel)
-    cfg = Config("edge", "fcc", 1, rc=1.0, rcs=0.5, sel=tuple(sel), widths=(1, 8, 16, m1),
-                 m2=m2, d1=d1, d2=d2)
-    nnei = sum(sel)
-    nlist = np.full((nloc, nnei), -1, np.int32)
-    em = np.zeros((nloc, nnei, 4))
-    x_up = lo + L1 * d1
-    x_end = x_up + L2 * d2
-    for i in range(nloc):
-        k = rng.integers(0, nnei + 1)
-        slots = rng.choice(nnei, size=k, replace=False)
-        nlist[i, slots] = rng.integers(0, nloc, size=k)
-        # slightly below lo (interval 0 extrapolated by less than a fifth of a
-        # step, where the quintic is still well conditioned), inside the range,
-        # in the band and past its end (clamped)
-        em[i, slots, 0] = rng.uniform(lo - 0.2 * d1, x_end + 0.5, size=k)
-        em[i, slots, 1:] = rng.normal(size=(k, 3))
-    atype = rng.integers(0, nt, size=nloc).astype(np.int32)
-    nets = [random_net(rng, cfg.widths) for _ in range(nt * nt)]
-    npair = nt * nt
-    return Inputs(cfg=cfg, atype=atype, nlist=nlist, em=em, nets=nets, lo=np.full(npair, lo),
-                  L1=np.full(npair, L1), L2=np.full(npair, L2), s_hat_max=np.zeros(npair),
-                  stats={}, dT=rng.normal(size=(nloc, m1, 4)), n_valid=int((nlist >= 0).sum()))
+def _synthetic(nloc, sel, m1, m2, seed, **kw):
+    """Hand-placed rows in every part of the tabulated range (below lo, main
+    range, band, past the band; fixed shares) for edge cases."""
+    from synth.edge import edge_inputs
+    return edge_inputs(nloc, sel, m1, m2, seed, **kw)
 
 
 @pytest.mark.parametrize("sel,m1,m2", [((3, 70), 100, 16), ((64,), 64, 64), ((5, 1, 60), 200, 7),
@@ -192,13 +195,50 @@ def test_empty_and_single_atom():
     assert T.shape == (0, 100, 4) and D.shape == (0, 100, 16) and dR.shape == (0, 40, 4)
 
 
-def test_nan_stays_in_its_atom():
+@pytest.mark.parametrize("col,val", [(1, np.nan), (0, np.nan), (0, np.inf), (0, -np.inf)])
+def test_nan_stays_in_its_atom(col, val):
+    # a non-finite entry of R~ makes the same outputs non-finite as in the
+    # oracle (a NaN or infinite first column is not silently clamped away)
+    # and no other atom's
     x = _synthetic(9, (50,), 100, 16, seed=4)
     j = int(np.nonzero(x.nlist[2] >= 0)[0][0])
-    x.em[2, j, 1] = np.nan
+    x.em[2, j, col] = val
     _, _, out = _run_gpu(x, "f64")
     T, D, dR = (t.cpu().numpy() for t in out)
-    assert np.isnan(T[2]).any()
+    assert not np.isfinite(T[2]).all()
     others = [i for i in range(9) if i != 2]
     assert np.isfinite(T[others]).all() and np.isfinite(D[others]).all() and np.isfinite(dR[others]).all()
     _check(x, np.array(others), (T, D, dR), "f64", with_bounds=False)
+    ref = oracle_fwd_bwd(x, np.array([2]), "f64")
+    for name, g, r in zip(("T", "D", "dR"), (T[2:3], D[2:3], dR[2:3]), ref):
+        np.testing.assert_array_equal(np.isfinite(g), np.isfinite(r), err_msg=name)
+        f = np.isfinite(r)
+        assert np.max(np.abs(g[f] - r[f])) <= 1e-12 * np.max(np.abs(r[f])), name
+
+
+@pytest.mark.parametrize("m1", [100, 17])
+def test_coefficients_past_the_buffer_are_not_read(m1):
+    # the coefficient tensor is a view into a larger allocation whose tail
+    # holds NaN; records in the last interval of the last type pair (clamped
+    # ones, a tenth of all) must not pick any of it up
+    import paper_2107_02103_amd as P
+    x = _synthetic(64, (40, 40), m1, 4, seed=m1)
+    c = x.cfg
+    op = P.SeATab(x.nets, x.lo, x.L1, x.L2, c.d1, c.d2, c.sel, c.m2)
+    n = op.coeff.numel()
+    big = torch.full((n + 4096,), float("nan"), dtype=torch.float64, device="cuda")
+    big[:n] = op.coeff
+    op.coeff = big[:n]
+    last = (x.atype == c.ntypes - 1)[:, None] & (np.arange(c.nnei) >= c.sel[0])[None, :]
+    x_end = x.lo[-1] + x.L1[-1] * c.d1 + x.L2[-1] * c.d2
+    assert np.sum(last & (x.nlist >= 0) & (x.em[..., 0] >= x_end)) > 20
+    em = torch.from_numpy(x.em).cuda()
+    nl = torch.from_numpy(x.nlist).cuda()
+    at = torch.from_numpy(x.atype).cuda()
+    dT = torch.from_numpy(x.dT).cuda()
+    T, D = op.forward(em, nl, at)
+    dR = op.backward(em, nl, at, dT)
+    torch.cuda.synchronize()
+    got = tuple(t.cpu().numpy() for t in (T, D, dR))
+    assert all(np.isfinite(g).all() for g in got)
+    _check(x, np.arange(64), got, "f64")
