@@ -11,8 +11,7 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-# DPC_LIBRARY may name another build of the same library (e.g. a tuning variant).
-LIB_PATH = os.environ.get("DPC_LIBRARY") or os.path.join(_HERE, "_lib", "libdpc.so")
+LIB_PATH = os.path.join(_HERE, "_lib", "libdpc.so")
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(
@@ -187,16 +186,34 @@ def build_tables(nets, ranges, dtype):
 
 
 def _ptr(x, dtype=None, name="?"):
-    """Device pointer of a contiguous torch tensor (or an int address)."""
+    """Device pointer of a contiguous torch tensor on a GPU (or an int
+    address, taken as is).  A tensor in host memory is refused: its address
+    would reach the kernels as a device address."""
     if x is None:
         return None
     if isinstance(x, int):
         return x
+    if not getattr(x, "is_cuda", False):
+        raise ValueError(f"{name} must be a tensor on a GPU device, not {getattr(x, 'device', type(x))}")
     if not x.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     if dtype is not None and x.dtype != dtype:
         raise TypeError(f"{name} has dtype {x.dtype}, expected {dtype}")
     return x.data_ptr()
+
+
+def _one_device(stream, **tensors):
+    """Every tensor argument (and a torch stream) must be on one GPU."""
+    devs = {k: v.device for k, v in tensors.items() if v is not None and not isinstance(v, int)}
+    for k, v in tensors.items():
+        if v is not None and not isinstance(v, int):
+            _ptr(v, name=k)
+    if stream is not None and not isinstance(stream, int) and hasattr(stream, "device"):
+        devs["stream"] = stream.device
+    idx = {(d.type, d.index) for d in devs.values()}
+    if len(idx) > 1:
+        raise ValueError("arguments on different devices: "
+                         + ", ".join(f"{k}={d}" for k, d in devs.items()))
 
 
 def _sel(sel):
@@ -232,6 +249,7 @@ def dpc_se_a_tab_fwd(stream, dtype, nloc, ntypes, sel, m1, m2, ranges, coeff, at
     nnei, (ei, eo) = sum(int(v) for v in sel), _io_sizes(dtype)
     _need(atype, nloc, 4, "atype"); _need(nlist, nloc * nnei, 4, "nlist")
     _need(em, nloc * nnei * 4, ei, "em"); _need(T, nloc * m1 * 4, eo, "T"); _need(D, nloc * m1 * m2, eo, "D")
+    _one_device(stream, coeff=coeff, atype=atype, nlist=nlist, em=em, T=T, D=D)
     _check(_lib.dpc_se_a_tab_fwd(_stream(stream), int(dtype), int(nloc), int(ntypes), _sel(sel),
                                  int(m1), int(m2), ranges, _ptr(coeff, name="coeff"),
                                  _ptr(atype, name="atype"), _ptr(nlist, name="nlist"),
@@ -245,6 +263,7 @@ def dpc_se_a_tab_bwd(stream, dtype, nloc, ntypes, sel, m1, ranges, coeff, atype,
     _need(atype, nloc, 4, "atype"); _need(nlist, nloc * nnei, 4, "nlist")
     _need(em, nloc * nnei * 4, ei, "em"); _need(dE_dT, nloc * m1 * 4, ei, "dE_dT")
     _need(dE_dem, nloc * nnei * 4, eo, "dE_dem")
+    _one_device(stream, coeff=coeff, atype=atype, nlist=nlist, em=em, dE_dT=dE_dT, dE_dem=dE_dem)
     _check(_lib.dpc_se_a_tab_bwd(_stream(stream), int(dtype), int(nloc), int(ntypes), _sel(sel),
                                  int(m1), ranges, _ptr(coeff, name="coeff"),
                                  _ptr(atype, name="atype"), _ptr(nlist, name="nlist"),
@@ -258,6 +277,7 @@ def dpc_descriptor_bwd(stream, dtype, nloc, m1, m2, T, dE_dD, dE_dT):
     eo = 8 if int(dtype) == DPC_F64 else 4
     _need(T, nloc * m1 * 4, ei, "T"); _need(dE_dD, nloc * m1 * m2, ei, "dE_dD")
     _need(dE_dT, nloc * m1 * 4, eo, "dE_dT")
+    _one_device(stream, T=T, dE_dD=dE_dD, dE_dT=dE_dT)
     _check(_lib.dpc_descriptor_bwd(_stream(stream), int(dtype), int(nloc), int(m1), int(m2),
                                    _ptr(T, name="T"), _ptr(dE_dD, name="dE_dD"),
                                    _ptr(dE_dT, name="dE_dT")),
@@ -278,6 +298,7 @@ def dpc_env_mat_a(stream, dtype, nloc, ntypes, nnei, box, rc, rcs, mean, sigma, 
     pa, ka = _dvec(sigma_all, ntypes, "sigma_all")
     _need(coord, nloc * 3, 8, "coord"); _need(atype, nloc, 4, "atype")
     _need(nlist, nloc * nnei, 4, "nlist"); _need(em, nloc * nnei * 4, 8 if int(dtype) == DPC_F64 else 4, "em")
+    _one_device(stream, coord=coord, atype=atype, nlist=nlist, em=em)
     _check(_lib.dpc_env_mat_a(_stream(stream), int(dtype), int(nloc), int(ntypes), int(nnei),
                               float(box), float(rc), float(rcs), pm, ps, pa, _ptr(coord, name="coord"),
                               _ptr(atype, name="atype"), _ptr(nlist, name="nlist"), _ptr(em, name="em")),
@@ -288,6 +309,7 @@ def dpc_nlist_reverse(stream, nloc, ntypes, sel, box, coord, atype, nlist, rev):
     nnei = sum(int(v) for v in sel)
     _need(coord, nloc * 3, 8, "coord"); _need(atype, nloc, 4, "atype")
     _need(nlist, nloc * nnei, 4, "nlist"); _need(rev, nloc * nnei, 4, "rev")
+    _one_device(stream, coord=coord, atype=atype, nlist=nlist, rev=rev)
     _check(_lib.dpc_nlist_reverse(_stream(stream), int(nloc), int(ntypes), _sel(sel), float(box),
                                   _ptr(coord, name="coord"), _ptr(atype, name="atype"),
                                   _ptr(nlist, name="nlist"), _ptr(rev, name="rev")),
@@ -302,6 +324,8 @@ def dpc_force_a(stream, dtype, nloc, ntypes, nnei, box, rc, rcs, sigma, sigma_al
     _need(nlist, nloc * nnei, 4, "nlist"); _need(rev, nloc * nnei, 4, "rev")
     _need(dE_dem, nloc * nnei * 4, 4 if int(dtype) == DPC_F32 else 8, "dE_dem")
     _need(force, nloc * 3, 8, "force"); _need(virial, nloc * 9, 8, "virial")
+    _one_device(stream, coord=coord, atype=atype, nlist=nlist, rev=rev, dE_dem=dE_dem, force=force,
+                virial=virial)
     _check(_lib.dpc_force_a(_stream(stream), int(dtype), int(nloc), int(ntypes), int(nnei),
                             float(box), float(rc), float(rcs), ps, pa, _ptr(coord, name="coord"),
                             _ptr(atype, name="atype"), _ptr(nlist, name="nlist"),
@@ -319,6 +343,7 @@ def dpc_fitting_fwd_bwd(stream, blas, nloc, net, D, workspace, workspace_bytes, 
     ``blas``: a rocblas_handle (int), see RocblasHandle."""
     _need(D, nloc * net.n_in, 8, "D"); _need(E, nloc, 8, "E"); _need(dE_dD, nloc * net.n_in, 8, "dE_dD")
     _need(workspace, workspace_bytes, 1, "workspace")
+    _one_device(stream, D=D, workspace=workspace, E=E, dE_dD=dE_dD)
     _check(_lib.dpc_fitting_fwd_bwd(_stream(stream), blas, int(nloc), C.byref(net), _ptr(D, name="D"),
                                     _ptr(workspace, name="workspace"), int(workspace_bytes),
                                     _ptr(E, name="E"), _ptr(dE_dD, name="dE_dD")),

@@ -252,11 +252,16 @@ def test_fitting_entry_point_validates_before_launch():
 def test_missing_library_fails_loudly(tmp_path):
     # the product path has no fallback: without the built library the first
     # use of any entry point raises ImportError
+    import shutil
     import subprocess
     import sys
+    pkg = tmp_path / "paper_2107_02103_amd"
+    pkg.mkdir()
+    for f in os.listdir(os.path.join(ROOT, "paper_2107_02103_amd")):
+        if f.endswith(".py"):                 # the package without its built _lib/
+            shutil.copy(os.path.join(ROOT, "paper_2107_02103_amd", f), pkg / f)
     code = "import paper_2107_02103_amd as P; P.dpc_version()"
-    env = dict(os.environ, DPC_LIBRARY=str(tmp_path / "absent" / "libdpc.so"))
-    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True, text=True,
+    r = subprocess.run([sys.executable, "-c", code], cwd=str(tmp_path), capture_output=True, text=True,
                        timeout=300)
     assert r.returncode != 0
     assert "ImportError" in r.stderr and "libdpc.so not found" in r.stderr
@@ -286,3 +291,31 @@ def test_binding_refuses_undersized_tensors():
         P.dpc_fitting_fwd_bwd(0, 1, 4, net, f64(64), f64(99), 800, f64(4))
     with pytest.raises(ValueError, match="nlist"):
         P.dpc_se_a_tab_fwd(0, P.DPC_F64, 2, 1, [5], 8, 4, None, 0, i32(2), i32(9), f64(40), f64(64), f64(64))
+
+
+def test_binding_refuses_host_tensors():
+    # a correctly sized tensor in host memory would pass its host address to
+    # the kernels: the binding refuses it before any call into the library
+    torch = pytest.importorskip("torch")
+    f64 = lambda n: torch.zeros(n, dtype=torch.float64)
+    i32 = lambda n: torch.zeros(n, dtype=torch.int32)
+    with pytest.raises(ValueError, match="GPU"):
+        P.dpc_descriptor_bwd(0, P.DPC_F64, 3, 8, 4, f64(3 * 8 * 4), f64(3 * 8 * 4), f64(3 * 8 * 4))
+    with pytest.raises(ValueError, match="GPU"):
+        P.dpc_se_a_tab_fwd(0, P.DPC_F64, 2, 1, [5], 8, 4, None, f64(8), i32(2), i32(10), f64(40),
+                           f64(64), f64(64))
+    with pytest.raises(ValueError, match="GPU"):
+        P.dpc_se_a_tab_bwd(0, P.DPC_F64, 2, 1, [5], 8, None, f64(8), i32(2), i32(10), f64(40),
+                           f64(64), f64(40))
+    with pytest.raises(ValueError, match="GPU"):
+        P.dpc_env_mat_a(0, P.DPC_F64, 2, 1, 5, 20.0, 6.0, 0.5, [0.0], [1.0], [1.0], f64(6), i32(2),
+                        i32(10), f64(40))
+    with pytest.raises(ValueError, match="GPU"):
+        P.dpc_nlist_reverse(0, 2, 1, [5], 20.0, f64(6), i32(2), i32(10), i32(10))
+    with pytest.raises(ValueError, match="GPU"):
+        P.dpc_force_a(0, P.DPC_F64, 2, 1, 5, 20.0, 6.0, 0.5, [1.0], [1.0], f64(6), i32(2), i32(10),
+                      i32(10), f64(40), f64(6), f64(18))
+    net = P.dpc_fitting_net()
+    net.n_in, net.width = 16, 8
+    with pytest.raises(ValueError, match="GPU"):
+        P.dpc_fitting_fwd_bwd(0, 1, 4, net, f64(64), f64(1000), 8000, f64(4))
