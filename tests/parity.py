@@ -1,6 +1,7 @@
-"""Shared helpers of the GPU parity tests and bench.py: run the library on a
-config's inputs and compare against the oracle.  The oracle side always
-starts from the same seeded inputs (``synth``) and builds its own tables."""
+"""Helpers of the GPU parity tests: the oracle's view of a workload's inputs
+and the comparisons (per-atom normwise and abs-sum-scaled componentwise).
+The oracle side always starts from the same seeded inputs (``synth``) and
+builds its own tables."""
 import numpy as np
 
 from oracle import cref
