@@ -213,7 +213,8 @@ def test_nan_stays_in_its_atom(col, val):
     for name, g, r in zip(("T", "D", "dR"), (T[2:3], D[2:3], dR[2:3]), ref):
         np.testing.assert_array_equal(np.isfinite(g), np.isfinite(r), err_msg=name)
         f = np.isfinite(r)
-        assert np.max(np.abs(g[f] - r[f])) <= 1e-12 * np.max(np.abs(r[f])), name
+        if f.any():
+            assert np.max(np.abs(g[f] - r[f])) <= 1e-12 * np.max(np.abs(r[f])), name
 
 
 @pytest.mark.parametrize("m1", [100, 17])
