@@ -15,7 +15,9 @@ arXiv:2107.02103, Sec. II) in float64:
                for the large workloads;
 * ``env``   -- the environment matrix R~ from positions (Eq. (1) and the
                normalisation) and the forces and virials from dE/dR~;
-* ``fitting`` -- the fitting net D -> E and its backward dE/dD.
+* ``fitting`` -- the fitting net D -> E and its backward dE/dD;
+* ``nlist`` -- the neighbour list (type blocks of sel slots, nearest first)
+               by brute force over all atom pairs, as plain C loops.
 
 It is test infrastructure only: the tests, ``__graft_entry__.smoke()`` and the
 ``cpu_baseline`` leg of ``bench.py`` may use it; the product path never does.
