@@ -39,6 +39,7 @@ extern "C" {
 #define DPC_ERANGE -2   /* bad table parameters: stride <= 0, L1 or L2 < 1, non-finite lo */
 #define DPC_EHIP -3     /* HIP runtime or launch error */
 #define DPC_ENOTSUP -4  /* supported but not implemented sizes (M1 > 256, ntypes > 8) */
+#define DPC_EOVERFLOW -5 /* a neighbour list had more atoms of some type within r_c than sel */
 
 #define DPC_MAX_TYPES 8
 #define DPC_MAX_M1 256
@@ -198,6 +199,44 @@ int dpc_env_mat_a(void* stream, dpc_dtype dtype, int nloc, int ntypes, int nnei,
  *   rev   device out int32 [nloc][nnei]                                      */
 int dpc_nlist_reverse(void* stream, int nloc, int ntypes, const int* sel, double box,
                       const double* coord, const int* atype, const int* nlist, int* rev);
+
+/* Bytes of device workspace dpc_nlist_build needs for nloc atoms in a cubic
+ * box of edge `box` with cutoff rc (the cell list: per-cell counters and
+ * offsets, and the atoms in cell order, 32 bytes each); 0 for bad sizes.   */
+size_t dpc_nlist_workspace_bytes(int nloc, double box, double rc);
+
+/* Neighbour list (paper Sec. II, the environment matrix: the neighbours of
+ * atom i within r_c, grouped by neighbour type into sel[beta] rows for type
+ * beta, sorted by distance inside a group, the unused rows empty):
+ *   - periodic cubic box of edge `box`, minimum image per component
+ *     d = x_j - x_i - box * rint((x_j - x_i) / box);
+ *   - r2 = dx*dx + dy*dy + dz*dz, each operation rounded on its own;
+ *   - j != i is a neighbour when r2 < rc*rc (and 0 <= atype[j] < ntypes);
+ *   - nlist[i][blk(beta) + k] = the k-th neighbour of type beta in the order
+ *     (r2, j) ascending, for k < sel[beta]; the remaining slots hold -1.
+ * The result does not depend on the order of the atoms inside the cell list
+ * (the order is total), so it is reproducible bitwise.
+ *   box, rc      require rc > 0 and box > 2 rc (else DPC_ERANGE)
+ *   sel          host [ntypes], ntypes <= DPC_MAX_TYPES
+ *   coord        device float64 [nloc][3] (any real values: positions are
+ *                wrapped into the box for the cell list only)
+ *   atype        device int32 [nloc]
+ *   workspace    device, 256-byte aligned, >= dpc_nlist_workspace_bytes()
+ *   nlist        device out int32 [nloc][sum(sel)] (the nlist input of the
+ *                calls above)
+ *   status_host  host int [2] or NULL.  With NULL the call is asynchronous
+ *                like the others; the two status counters it leaves in the
+ *                first 8 bytes of the workspace are the numbers of atoms
+ *                whose list was truncated (some type had more than sel
+ *                neighbours: its nearest sel are kept) and of atoms with
+ *                more than 1024 atoms within rc (their list is incomplete).
+ *                With a host array the call waits for its kernels, copies
+ *                the two counters there and returns DPC_EOVERFLOW if the
+ *                first is nonzero, DPC_ENOTSUP if the second is.
+ * nloc = 0 is a no-op.  Errors and ownership as the calls above.            */
+int dpc_nlist_build(void* stream, int nloc, int ntypes, const int* sel, double box, double rc,
+                    const double* coord, const int* atype, void* workspace,
+                    size_t workspace_bytes, int* nlist, int* status_host);
 
 /* Forces and per-atom virials from dE/dR~ (F = -dE/dr; paper Sec. II: the
  * forces need the derivatives of E with respect to R~).  With

@@ -27,12 +27,13 @@ except ImportError:  # the C library can be used without torch
     torch = None
 _lib = C.CDLL(LIB_PATH)
 
-DPC_OK, DPC_EINVAL, DPC_ERANGE, DPC_EHIP, DPC_ENOTSUP = 0, -1, -2, -3, -4
+DPC_OK, DPC_EINVAL, DPC_ERANGE, DPC_EHIP, DPC_ENOTSUP, DPC_EOVERFLOW = 0, -1, -2, -3, -4, -5
 DPC_F64, DPC_F32, DPC_F32_ACC64 = 0, 1, 2
 DPC_MAX_TYPES, DPC_MAX_M1 = 8, 256
 EXPORTED = ("dpc_strerror", "dpc_last_hip_error", "dpc_version", "dpc_table_layout", "dpc_build_table",
             "dpc_se_a_tab_fwd", "dpc_se_a_tab_bwd", "dpc_descriptor_bwd", "dpc_env_mat_a",
-            "dpc_nlist_reverse", "dpc_force_a", "dpc_fitting_workspace_bytes", "dpc_fitting_fwd_bwd")
+            "dpc_nlist_reverse", "dpc_force_a", "dpc_fitting_workspace_bytes", "dpc_fitting_fwd_bwd",
+            "dpc_nlist_workspace_bytes", "dpc_nlist_build")
 
 
 class dpc_range(C.Structure):
@@ -84,6 +85,11 @@ _lib.dpc_force_a.restype = C.c_int
 _lib.dpc_force_a.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_int, _D, _D, _D,
                              C.POINTER(_D), C.POINTER(_D), C.c_void_p, C.c_void_p, C.c_void_p,
                              C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+_lib.dpc_nlist_workspace_bytes.restype = C.c_size_t
+_lib.dpc_nlist_workspace_bytes.argtypes = [C.c_int, _D, _D]
+_lib.dpc_nlist_build.restype = C.c_int
+_lib.dpc_nlist_build.argtypes = [C.c_void_p, C.c_int, C.c_int, C.POINTER(C.c_int), _D, _D, C.c_void_p,
+                                 C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p, C.POINTER(C.c_int)]
 _lib.dpc_descriptor_bwd.restype = C.c_int
 _lib.dpc_descriptor_bwd.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p,
                                     C.c_void_p, C.c_void_p]
@@ -332,6 +338,27 @@ def dpc_force_a(stream, dtype, nloc, ntypes, nnei, box, rc, rcs, sigma, sigma_al
                             _ptr(rev, name="rev"), _ptr(dE_dem, name="dE_dem"),
                             _ptr(force, name="force"), _ptr(virial, name="virial")),
            "dpc_force_a")
+
+
+def dpc_nlist_workspace_bytes(nloc, box, rc):
+    return int(_lib.dpc_nlist_workspace_bytes(int(nloc), float(box), float(rc)))
+
+
+def dpc_nlist_build(stream, nloc, ntypes, sel, box, rc, coord, atype, workspace, workspace_bytes, nlist,
+                    wait=True):
+    """Neighbour list into ``nlist``.  With ``wait`` the call synchronises and
+    returns the two status counters (truncated lists, lists over capacity),
+    raising DpcError for either; without, it returns None."""
+    nnei = sum(int(v) for v in sel)
+    _need(coord, nloc * 3, 8, "coord"); _need(atype, nloc, 4, "atype")
+    _need(workspace, workspace_bytes, 1, "workspace"); _need(nlist, nloc * nnei, 4, "nlist")
+    _one_device(stream, coord=coord, atype=atype, workspace=workspace, nlist=nlist)
+    st = (C.c_int * 2)(0, 0) if wait else None
+    _check(_lib.dpc_nlist_build(_stream(stream), int(nloc), int(ntypes), _sel(sel), float(box), float(rc),
+                                _ptr(coord, name="coord"), _ptr(atype, name="atype"),
+                                _ptr(workspace, name="workspace"), int(workspace_bytes),
+                                _ptr(nlist, name="nlist"), st), "dpc_nlist_build")
+    return (st[0], st[1]) if wait else None
 
 
 def dpc_fitting_workspace_bytes(nloc, width):

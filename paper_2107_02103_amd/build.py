@@ -16,7 +16,8 @@ LIB_DIR = os.path.join(HERE, "_lib")
 LIB = os.path.join(LIB_DIR, "libdpc.so")
 ARCH = "gfx950"
 
-SOURCES = ["dpc_table.cpp", "dpc_se_a.hip", "dpc_descriptor.hip", "dpc_env.hip", "dpc_fitting.hip"]
+SOURCES = ["dpc_table.cpp", "dpc_se_a.hip", "dpc_descriptor.hip", "dpc_env.hip", "dpc_fitting.hip",
+           "dpc_nlist.hip"]
 
 # packed fp32 instructions are disabled for all device code
 HIPCC_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

@@ -1,0 +1,359 @@
+// Neighbour list of a periodic cubic box (DP Compress, Sec. II: the rows of
+// the environment matrix are the neighbours within r_c, grouped by type into
+// sel_beta rows each, sorted by distance inside a group, unused rows empty).
+//
+// Definition (the same as the plain oracle's): minimum image per component,
+// d = x_j - x_i - box rint((x_j - x_i) / box); r2 = dx dx + dy dy + dz dz,
+// every operation rounded on its own; j != i is a neighbour when
+// r2 < rc * rc; neighbours are ordered by (type, r2, j) and the first
+// sel[beta] of type beta fill block beta; empty slots hold -1.
+//
+// Cell list: cells of edge box / nc >= r_c (slightly more, so that rounding
+// at a cell face cannot put two atoms closer than r_c two cells apart).
+//   1. zero the counters;  2. cell of each atom, counted with atomics;
+//   3. exclusive scan (one workgroup);  4. scatter the atoms into cell order
+//   with their coordinates, index and type packed in 32 bytes;
+//   5. one wavefront per atom walks the (up to) 27 cells around its own,
+//   64 candidates at a time, keeps those within r_c in LDS, ranks each of
+//   them among the candidates of its type and writes its slot.
+// The order inside a cell depends on the atomics, but the ranking is a total
+// order, so the list does not.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "dpc.h"
+#include "dpc_internal.h"
+
+namespace {
+
+constexpr int kNlWaves = 4;      // wavefronts (atoms) per workgroup of the list kernel
+constexpr int kNlCap = 1024;     // neighbours within rc one wavefront keeps (16 KB of LDS)
+constexpr int kScanThreads = 1024;
+
+struct alignas(16) NlAtom {      // an atom in cell order
+  double x, y, z;
+  int j, type;
+};
+
+struct alignas(16) NlCand {      // a neighbour within r_c, as kept in LDS
+  uint64_t r2;                   // bits of r2 (>= 0: ordered like the value)
+  int j, type;
+};
+
+struct NlGeo {
+  int nloc, ntypes, nnei, nc, ncell;
+  int lo_off, n_off;             // stencil offsets per axis: lo_off .. lo_off + n_off - 1
+  double box, rc2, inv_cs;
+  int sel[DPC_MAX_TYPES];
+  int blk[DPC_MAX_TYPES + 1];    // first slot of each type block
+};
+
+__device__ __forceinline__ double min_image(double d, double box) {
+#pragma clang fp contract(off)
+  return d - box * rint(d / box);
+}
+
+__device__ __forceinline__ int cell_axis(double x, const NlGeo& g) {
+#pragma clang fp contract(off)
+  const double w = x - g.box * floor(x / g.box);       // into [0, box]
+  // clamped as a double first: NaN and infinite positions land in cell 0
+  return (int)fmin(fmax(w * g.inv_cs, 0.0), (double)(g.nc - 1));
+}
+
+__global__ void nl_zero_kernel(int n, int* __restrict__ p) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+__global__ void nl_cell_kernel(const NlGeo g, const double* __restrict__ coord,
+                               int* __restrict__ count, int* __restrict__ cell_of) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= g.nloc) return;
+  const double* p = coord + 3 * (size_t)i;
+  const int c = (cell_axis(p[0], g) * g.nc + cell_axis(p[1], g)) * g.nc + cell_axis(p[2], g);
+  cell_of[i] = c;
+  atomicAdd(count + c, 1);
+}
+
+// exclusive scan of count[0..ncell) into start[0..ncell] and cursor[0..ncell)
+__global__ __launch_bounds__(kScanThreads) void nl_scan_kernel(int ncell,
+                                                               const int* __restrict__ count,
+                                                               int* __restrict__ start,
+                                                               int* __restrict__ cursor) {
+  __shared__ int part[kScanThreads];
+  const int t = threadIdx.x;
+  const int per = (ncell + kScanThreads - 1) / kScanThreads;
+  const int c0 = min(ncell, t * per), c1 = min(ncell, c0 + per);
+  int sum = 0;
+  for (int c = c0; c < c1; ++c) sum += count[c];
+  part[t] = sum;
+  __syncthreads();
+  for (int off = 1; off < kScanThreads; off <<= 1) {   // inclusive scan of the parts
+    const int v = t >= off ? part[t - off] : 0;
+    __syncthreads();
+    part[t] += v;
+    __syncthreads();
+  }
+  int run = part[t] - sum;
+  for (int c = c0; c < c1; ++c) {
+    start[c] = run;
+    cursor[c] = run;
+    run += count[c];
+  }
+  if (t == kScanThreads - 1) start[ncell] = part[t];
+}
+
+__global__ void nl_scatter_kernel(const NlGeo g, const double* __restrict__ coord,
+                                  const int* __restrict__ atype,
+                                  const int* __restrict__ cell_of, int* __restrict__ cursor,
+                                  NlAtom* __restrict__ sorted) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= g.nloc) return;
+  const int p = atomicAdd(cursor + cell_of[i], 1);
+  const double* c = coord + 3 * (size_t)i;
+  NlAtom a;
+  a.x = c[0];
+  a.y = c[1];
+  a.z = c[2];
+  a.j = i;
+  a.type = atype[i];
+  sorted[p] = a;
+}
+
+__device__ __forceinline__ uint64_t ballot(bool b) { return __ballot(b); }
+
+__device__ __forceinline__ int lanes_below(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+}
+
+// one wavefront per atom
+__global__ __launch_bounds__(64 * kNlWaves) void nl_list_kernel(
+    const NlGeo g, const double* __restrict__ coord, const int* __restrict__ cell_of,
+    const int* __restrict__ start, const NlAtom* __restrict__ sorted, int* __restrict__ nlist,
+    int* __restrict__ status) {
+#pragma clang fp contract(off)
+  __shared__ NlCand cand[kNlWaves][kNlCap];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = __builtin_amdgcn_readfirstlane((int)(blockIdx.x * kNlWaves + wave));
+  if (i >= g.nloc) return;
+  NlCand* my = cand[wave];
+  const double xi = coord[3 * (size_t)i], yi = coord[3 * (size_t)i + 1], zi = coord[3 * (size_t)i + 2];
+  const int ci = __builtin_amdgcn_readfirstlane(cell_of[i]);
+  const int cx = ci / (g.nc * g.nc), cy = (ci / g.nc) % g.nc, cz = ci % g.nc;
+
+  // candidates within rc, in the order they are met (n may pass kNlCap:
+  // the extra ones are counted, not kept)
+  int n = 0;
+  for (int ox = 0; ox < g.n_off; ++ox)
+    for (int oy = 0; oy < g.n_off; ++oy)
+      for (int oz = 0; oz < g.n_off; ++oz) {
+        const int ax = (cx + g.lo_off + ox + g.nc) % g.nc;
+        const int ay = (cy + g.lo_off + oy + g.nc) % g.nc;
+        const int az = (cz + g.lo_off + oz + g.nc) % g.nc;
+        const int c = (ax * g.nc + ay) * g.nc + az;
+        const int p0 = start[c], p1 = start[c + 1];
+        for (int b = p0; b < p1; b += 64) {
+          const int p = b + lane;
+          bool ok = false;
+          NlCand k{0, 0, 0};
+          if (p < p1) {
+            const NlAtom a = sorted[p];
+            const double dx = min_image(a.x - xi, g.box);
+            const double dy = min_image(a.y - yi, g.box);
+            const double dz = min_image(a.z - zi, g.box);
+            const double r2 = dx * dx + dy * dy + dz * dz;
+            ok = r2 < g.rc2 && a.j != i && a.type >= 0 && a.type < g.ntypes;
+            k.r2 = __builtin_bit_cast(uint64_t, r2);
+            k.j = a.j;
+            k.type = a.type;
+          }
+          const uint64_t m = ballot(ok);
+          const int pos = n + lanes_below(m);
+          if (ok && pos < kNlCap) my[pos] = k;
+          n += __popcll(m);
+        }
+      }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const int m = n < kNlCap ? n : kNlCap;
+
+  // neighbours of each type (all of them, before truncation)
+  int cnt[DPC_MAX_TYPES];
+#pragma unroll
+  for (int t = 0; t < DPC_MAX_TYPES; ++t) cnt[t] = 0;
+  for (int b = 0; b < m; b += 64) {
+    const int q = b + lane;
+    const int ty = q < m ? my[q].type : -1;
+#pragma unroll
+    for (int t = 0; t < DPC_MAX_TYPES; ++t) cnt[t] += __popcll(ballot(ty == t));
+  }
+
+  // slot of each kept neighbour: its rank among the neighbours of its type,
+  // by (r2, j); four candidates per lane per pass over all m
+  int* row = nlist + (size_t)i * g.nnei;
+  for (int b = 0; b < m; b += 256) {
+    NlCand own[4];
+    int rank[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int q = b + 64 * u + lane;
+      own[u] = q < m ? my[q] : NlCand{~0ull, -1, -1};
+      rank[u] = 0;
+    }
+    for (int e = 0; e < m; ++e) {
+      const NlCand o = my[e];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        rank[u] += (o.type == own[u].type &&
+                    (o.r2 < own[u].r2 || (o.r2 == own[u].r2 && o.j < own[u].j))) ? 1 : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int t = own[u].type;
+      if (t >= 0 && rank[u] < g.sel[t]) row[g.blk[t] + rank[u]] = own[u].j;
+    }
+  }
+  // empty slots of each block
+  for (int s = lane; s < g.nnei; s += 64) {
+    int t = 0;
+#pragma unroll
+    for (int u = 1; u < DPC_MAX_TYPES; ++u) t += (u < g.ntypes && s >= g.blk[u]) ? 1 : 0;
+    int c = 0;
+#pragma unroll
+    for (int u = 0; u < DPC_MAX_TYPES; ++u) c = u == t ? cnt[u] : c;
+    if (s - g.blk[t] >= c) row[s] = -1;
+  }
+  if (lane == 0) {
+    bool trunc = false;
+#pragma unroll
+    for (int t = 0; t < DPC_MAX_TYPES; ++t) trunc |= t < g.ntypes && cnt[t] > g.sel[t];
+    if (trunc) atomicAdd(status, 1);
+    if (n > kNlCap) atomicAdd(status + 1, 1);
+  }
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// cells per axis: edge >= rc (1 + 1e-9); at most 1024 per axis and 8 cells per atom
+int cells_per_axis(int nloc, double box, double rc) {
+  double n = std::floor(box / (rc * (1.0 + 1e-9)));
+  if (!(n >= 1.0)) n = 1.0;
+  if (n > 1024.0) n = 1024.0;
+  const double cap = std::max(64.0, 8.0 * nloc);
+  while (n > 1.0 && n * n * n > cap) n -= 1.0;
+  return (int)n;
+}
+
+struct NlLayout {
+  size_t status, count, start, cursor, cell_of, sorted, total;
+};
+
+NlLayout layout(int nloc, int ncell) {
+  NlLayout L;
+  size_t o = 0;
+  L.status = o; o += align256(2 * sizeof(int));
+  L.count = o; o += align256((size_t)ncell * sizeof(int));
+  L.start = o; o += align256(((size_t)ncell + 1) * sizeof(int));
+  L.cursor = o; o += align256((size_t)ncell * sizeof(int));
+  L.cell_of = o; o += align256((size_t)nloc * sizeof(int));
+  L.sorted = o; o += align256((size_t)nloc * sizeof(NlAtom));
+  L.total = o;
+  return L;
+}
+
+int make_geo(int nloc, int ntypes, const int* sel, double box, double rc, NlGeo* g) {
+#pragma clang fp contract(off)
+  if (nloc < 0 || ntypes < 1 || !sel) return DPC_EINVAL;
+  if (ntypes > DPC_MAX_TYPES) return DPC_ENOTSUP;
+  if (!(std::isfinite(box) && std::isfinite(rc) && rc > 0.0 && box > 2.0 * rc)) return DPC_ERANGE;
+  int64_t nnei = 0;
+  for (int t = 0; t < ntypes; ++t) {
+    if (sel[t] < 0) return DPC_EINVAL;
+    g->blk[t] = (int)nnei;
+    g->sel[t] = sel[t];
+    nnei += sel[t];
+  }
+  if (nnei < 1 || nnei > (1 << 20)) return DPC_EINVAL;
+  for (int t = ntypes; t < DPC_MAX_TYPES; ++t) g->sel[t] = 0;
+  for (int t = ntypes; t <= DPC_MAX_TYPES; ++t) g->blk[t] = (int)nnei;
+  g->nloc = nloc;
+  g->ntypes = ntypes;
+  g->nnei = (int)nnei;
+  g->nc = cells_per_axis(nloc, box, rc);
+  g->ncell = g->nc * g->nc * g->nc;
+  g->lo_off = g->nc >= 3 ? -1 : 0;
+  g->n_off = g->nc >= 3 ? 3 : g->nc;
+  g->box = box;
+  g->rc2 = rc * rc;
+  g->inv_cs = g->nc / box;
+  return DPC_OK;
+}
+
+}  // namespace
+
+size_t dpc_nlist_scratch_bytes(int nloc, double box, double rc) {
+  if (nloc < 0 || !(std::isfinite(box) && std::isfinite(rc) && rc > 0.0 && box > 2.0 * rc)) return 0;
+  const int nc = cells_per_axis(nloc, box, rc);
+  return layout(nloc, nc * nc * nc).total;
+}
+
+int dpc_nlist_launch(void* stream, int nloc, int ntypes, const int* sel, double box, double rc,
+                     const double* coord, const int* atype, void* workspace,
+                     size_t workspace_bytes, int* nlist, int* status_host) {
+  NlGeo g;
+  const int st = make_geo(nloc, ntypes, sel, box, rc, &g);
+  if (st != DPC_OK) return st;
+  if (nloc == 0) {
+    if (status_host) status_host[0] = status_host[1] = 0;
+    return DPC_OK;
+  }
+  if (!coord || !atype || !workspace || !nlist) return DPC_EINVAL;
+  const NlLayout L = layout(nloc, g.ncell);
+  if (workspace_bytes < L.total || reinterpret_cast<uintptr_t>(workspace) % 256) return DPC_EINVAL;
+  unsigned char* w = static_cast<unsigned char*>(workspace);
+  int* status = reinterpret_cast<int*>(w + L.status);
+  int* count = reinterpret_cast<int*>(w + L.count);
+  int* start = reinterpret_cast<int*>(w + L.start);
+  int* cursor = reinterpret_cast<int*>(w + L.cursor);
+  int* cell_of = reinterpret_cast<int*>(w + L.cell_of);
+  NlAtom* sorted = reinterpret_cast<NlAtom*>(w + L.sorted);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();  // report only what these launches raise
+  // the counters and the status words start at zero (a fill kernel, not a memset)
+  hipLaunchKernelGGL(nl_zero_kernel, dim3(1), dim3(64), 0, s, 2, status);
+  hipLaunchKernelGGL(nl_zero_kernel, dim3((g.ncell + 255) / 256), dim3(256), 0, s, g.ncell, count);
+  const dim3 ga((nloc + 255) / 256), b256(256);
+  hipLaunchKernelGGL(nl_cell_kernel, ga, b256, 0, s, g, coord, count, cell_of);
+  hipLaunchKernelGGL(nl_scan_kernel, dim3(1), dim3(kScanThreads), 0, s, g.ncell, count, start, cursor);
+  hipLaunchKernelGGL(nl_scatter_kernel, ga, b256, 0, s, g, coord, atype, cell_of, cursor, sorted);
+  hipLaunchKernelGGL(nl_list_kernel, dim3((nloc + kNlWaves - 1) / kNlWaves), dim3(64 * kNlWaves), 0, s,
+                     g, coord, cell_of, start, sorted, nlist, status);
+  const int ls = dpc_internal_launch_status();
+  if (ls != DPC_OK || !status_host) return ls;
+  int h[2] = {0, 0};
+  if (hipMemcpyAsync(h, status, sizeof h, hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess) {
+    const int e = dpc_internal_launch_status();   // keeps the HIP error for dpc_last_hip_error
+    return e == DPC_OK ? DPC_EHIP : e;
+  }
+  status_host[0] = h[0];
+  status_host[1] = h[1];
+  if (h[1] > 0) return DPC_ENOTSUP;
+  if (h[0] > 0) return DPC_EOVERFLOW;
+  return DPC_OK;
+}
+
+extern "C" size_t dpc_nlist_workspace_bytes(int nloc, double box, double rc) {
+  return dpc_nlist_scratch_bytes(nloc, box, rc);
+}
+
+extern "C" int dpc_nlist_build(void* stream, int nloc, int ntypes, const int* sel, double box,
+                               double rc, const double* coord, const int* atype, void* workspace,
+                               size_t workspace_bytes, int* nlist, int* status_host) {
+  return dpc_nlist_launch(stream, nloc, ntypes, sel, box, rc, coord, atype, workspace,
+                          workspace_bytes, nlist, status_host);
+}

@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_strerror_and_version():
     assert P.dpc_version() >= 100
-    for s in (0, -1, -2, -3, -4):
+    for s in (0, -1, -2, -3, -4, -5):
         assert len(P.dpc_strerror(s)) > 1
     assert P.dpc_strerror(-99) == "unknown status"
 
@@ -319,3 +319,23 @@ def test_binding_refuses_host_tensors():
     net.n_in, net.width = 16, 8
     with pytest.raises(ValueError, match="GPU"):
         P.dpc_fitting_fwd_bwd(0, 1, 4, net, f64(64), f64(1000), 8000, f64(4))
+
+
+def test_nlist_entry_point_validates_before_launch():
+    fake = 4096
+    nb = P.dpc_nlist_workspace_bytes(100, 20.0, 5.0)
+    assert nb > 100 * 32 and nb % 256 == 0
+    assert P.dpc_nlist_workspace_bytes(100, 10.0, 5.0) == 0       # box not above 2 rc
+    assert P.dpc_nlist_workspace_bytes(-1, 20.0, 5.0) == 0
+    base = dict(stream=0, nloc=100, ntypes=2, sel=[8, 8], box=20.0, rc=5.0, coord=fake, atype=fake,
+                workspace=fake * 256, workspace_bytes=nb, nlist=fake, wait=False)
+    cases = [(dict(box=10.0), B.DPC_ERANGE), (dict(rc=0.0), B.DPC_ERANGE), (dict(rc=float("nan")), B.DPC_ERANGE),
+             (dict(nloc=-1), B.DPC_EINVAL), (dict(sel=[8, -1]), B.DPC_EINVAL), (dict(coord=0), B.DPC_EINVAL),
+             (dict(workspace_bytes=nb - 1), B.DPC_EINVAL), (dict(workspace=fake * 256 + 16), B.DPC_EINVAL),
+             (dict(ntypes=9, sel=[1] * 9), B.DPC_ENOTSUP), (dict(nlist=0), B.DPC_EINVAL)]
+    for kw, code in cases:
+        a = dict(base); a.update(kw)
+        with pytest.raises(P.DpcError) as e:
+            P.dpc_nlist_build(**a)
+        assert e.value.status == code, kw
+    assert P.dpc_nlist_build(**{**base, "nloc": 0, "coord": 0, "nlist": 0, "wait": True}) == (0, 0)
