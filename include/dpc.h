@@ -238,6 +238,25 @@ int dpc_nlist_build(void* stream, int nloc, int ntypes, const int* sel, double b
                     const double* coord, const int* atype, void* workspace,
                     size_t workspace_bytes, int* nlist, int* status_host);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid hipMalloc): dpc_nlist_build
+ * with its cell list kept in a static device array of the library instead of
+ * a caller's workspace.  The call allocates nothing and never waits.  Each
+ * GPU it runs on holds one copy of that array (about 25 MB: the layout for
+ * DPC_NLIST_NOALLOC_MAX_ATOMS atoms) until the process ends.
+ *   nloc    at most DPC_NLIST_NOALLOC_MAX_ATOMS (else DPC_ENOTSUP)
+ *   stream  must run on the current device (else DPC_EINVAL)
+ *   status  device out int [2] or NULL: the two counters of dpc_nlist_build
+ *           (truncated lists, lists over capacity), written by the kernels
+ * All calls on one GPU share the array and every call starts by clearing
+ * its counters and overwrites the rest: calls that overlap in time on one
+ * GPU (other streams, other host threads) race, and the caller must
+ * serialise them.  Other arguments, results and errors as dpc_nlist_build. */
+#define DPC_NLIST_NOALLOC_MAX_ATOMS 524288
+int dpc_nlist_build_noalloc(void* stream, int nloc, int ntypes, const int* sel, double box,
+                            double rc, const double* coord, const int* atype, int* nlist,
+                            int* status);
+
 /* Forces and per-atom virials from dE/dR~ (F = -dE/dr; paper Sec. II: the
  * forces need the derivatives of E with respect to R~).  With
  * g_is = dE/dr_ij = sum_c dE/dR~_is[c] dR~_is[c]/dr_ij (dR~/dr from the

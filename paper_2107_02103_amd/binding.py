@@ -30,10 +30,11 @@ _lib = C.CDLL(LIB_PATH)
 DPC_OK, DPC_EINVAL, DPC_ERANGE, DPC_EHIP, DPC_ENOTSUP, DPC_EOVERFLOW = 0, -1, -2, -3, -4, -5
 DPC_F64, DPC_F32, DPC_F32_ACC64 = 0, 1, 2
 DPC_MAX_TYPES, DPC_MAX_M1 = 8, 256
+DPC_NLIST_NOALLOC_MAX_ATOMS = 524288
 EXPORTED = ("dpc_strerror", "dpc_last_hip_error", "dpc_version", "dpc_table_layout", "dpc_build_table",
             "dpc_se_a_tab_fwd", "dpc_se_a_tab_bwd", "dpc_descriptor_bwd", "dpc_env_mat_a",
             "dpc_nlist_reverse", "dpc_force_a", "dpc_fitting_workspace_bytes", "dpc_fitting_fwd_bwd",
-            "dpc_nlist_workspace_bytes", "dpc_nlist_build")
+            "dpc_nlist_workspace_bytes", "dpc_nlist_build", "dpc_nlist_build_noalloc")
 
 
 class dpc_range(C.Structure):
@@ -90,6 +91,9 @@ _lib.dpc_nlist_workspace_bytes.argtypes = [C.c_int, _D, _D]
 _lib.dpc_nlist_build.restype = C.c_int
 _lib.dpc_nlist_build.argtypes = [C.c_void_p, C.c_int, C.c_int, C.POINTER(C.c_int), _D, _D, C.c_void_p,
                                  C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p, C.POINTER(C.c_int)]
+_lib.dpc_nlist_build_noalloc.restype = C.c_int
+_lib.dpc_nlist_build_noalloc.argtypes = [C.c_void_p, C.c_int, C.c_int, C.POINTER(C.c_int), _D, _D,
+                                         C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
 _lib.dpc_descriptor_bwd.restype = C.c_int
 _lib.dpc_descriptor_bwd.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p,
                                     C.c_void_p, C.c_void_p]
@@ -359,6 +363,19 @@ def dpc_nlist_build(stream, nloc, ntypes, sel, box, rc, coord, atype, workspace,
                                 _ptr(workspace, name="workspace"), int(workspace_bytes),
                                 _ptr(nlist, name="nlist"), st), "dpc_nlist_build")
     return (st[0], st[1]) if wait else None
+
+
+def dpc_nlist_build_noalloc(stream, nloc, ntypes, sel, box, rc, coord, atype, nlist, status=None):
+    """dpc_nlist_build with the library's static cell list (no allocation,
+    asynchronous); ``status``: a device int32 tensor of 2 for the counters."""
+    nnei = sum(int(v) for v in sel)
+    _need(coord, nloc * 3, 8, "coord"); _need(atype, nloc, 4, "atype")
+    _need(nlist, nloc * nnei, 4, "nlist"); _need(status, 2, 4, "status")
+    _one_device(stream, coord=coord, atype=atype, nlist=nlist, status=status)
+    _check(_lib.dpc_nlist_build_noalloc(_stream(stream), int(nloc), int(ntypes), _sel(sel), float(box),
+                                        float(rc), _ptr(coord, name="coord"), _ptr(atype, name="atype"),
+                                        _ptr(nlist, name="nlist"), _ptr(status, name="status")),
+           "dpc_nlist_build_noalloc")
 
 
 def dpc_fitting_workspace_bytes(nloc, width):

@@ -23,6 +23,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 
 #include "dpc.h"
 #include "dpc_internal.h"
@@ -236,14 +237,14 @@ __global__ __launch_bounds__(64 * kNlWaves) void nl_list_kernel(
   }
 }
 
-size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+constexpr size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-// cells per axis: edge >= rc (1 + 1e-9); at most 1024 per axis and 8 cells per atom
+// cells per axis: edge >= rc (1 + 1e-9); at most 1024 per axis and one cell per atom
 int cells_per_axis(int nloc, double box, double rc) {
   double n = std::floor(box / (rc * (1.0 + 1e-9)));
   if (!(n >= 1.0)) n = 1.0;
   if (n > 1024.0) n = 1024.0;
-  const double cap = std::max(64.0, 8.0 * nloc);
+  const double cap = std::max(64.0, (double)nloc);
   while (n > 1.0 && n * n * n > cap) n -= 1.0;
   return (int)n;
 }
@@ -252,8 +253,8 @@ struct NlLayout {
   size_t status, count, start, cursor, cell_of, sorted, total;
 };
 
-NlLayout layout(int nloc, int ncell) {
-  NlLayout L;
+constexpr NlLayout layout(int nloc, int ncell) {
+  NlLayout L{};
   size_t o = 0;
   L.status = o; o += align256(2 * sizeof(int));
   L.count = o; o += align256((size_t)ncell * sizeof(int));
@@ -295,15 +296,18 @@ int make_geo(int nloc, int ntypes, const int* sel, double box, double rc, NlGeo*
 
 }  // namespace
 
-size_t dpc_nlist_scratch_bytes(int nloc, double box, double rc) {
+static size_t dpc_nlist_scratch_bytes(int nloc, double box, double rc) {
   if (nloc < 0 || !(std::isfinite(box) && std::isfinite(rc) && rc > 0.0 && box > 2.0 * rc)) return 0;
   const int nc = cells_per_axis(nloc, box, rc);
   return layout(nloc, nc * nc * nc).total;
 }
 
-int dpc_nlist_launch(void* stream, int nloc, int ntypes, const int* sel, double box, double rc,
-                     const double* coord, const int* atype, void* workspace,
-                     size_t workspace_bytes, int* nlist, int* status_host) {
+// status_dev: device int[2] for the two counters (NULL: the first 8 bytes of
+// the workspace); status_host: host int[2] to wait for and copy them to, or NULL
+static int dpc_nlist_launch(void* stream, int nloc, int ntypes, const int* sel, double box, double rc,
+                            const double* coord, const int* atype, void* workspace,
+                            size_t workspace_bytes, int* nlist, int* status_dev,
+                            int* status_host) {
   NlGeo g;
   const int st = make_geo(nloc, ntypes, sel, box, rc, &g);
   if (st != DPC_OK) return st;
@@ -315,7 +319,7 @@ int dpc_nlist_launch(void* stream, int nloc, int ntypes, const int* sel, double 
   const NlLayout L = layout(nloc, g.ncell);
   if (workspace_bytes < L.total || reinterpret_cast<uintptr_t>(workspace) % 256) return DPC_EINVAL;
   unsigned char* w = static_cast<unsigned char*>(workspace);
-  int* status = reinterpret_cast<int*>(w + L.status);
+  int* status = status_dev ? status_dev : reinterpret_cast<int*>(w + L.status);
   int* count = reinterpret_cast<int*>(w + L.count);
   int* start = reinterpret_cast<int*>(w + L.start);
   int* cursor = reinterpret_cast<int*>(w + L.cursor);
@@ -347,6 +351,70 @@ int dpc_nlist_launch(void* stream, int nloc, int ntypes, const int* sel, double 
   return DPC_OK;
 }
 
+// ---------------------------------------------------------------------------
+// The same list with the cell list in a static device array of the library,
+// for callers that cannot allocate device memory.  Each GPU that runs it
+// holds one copy of the array until the process ends; host code reaches it
+// only through the device address hipGetSymbolAddress gives for that GPU.
+// ---------------------------------------------------------------------------
+// the cell count is capped at max(64, nloc): the largest layout is that of
+// DPC_NLIST_NOALLOC_MAX_ATOMS atoms and as many cells
+static constexpr size_t kScratchBytes =
+    layout(DPC_NLIST_NOALLOC_MAX_ATOMS, DPC_NLIST_NOALLOC_MAX_ATOMS).total;
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// device address of this GPU's copy of `scratch`, looked up once per device
+// with that device current
+int scratch_address(int dev, void** out) {
+  if (dev < 0 || dev >= kMaxDevices) return DPC_ENOTSUP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      const int e = dpc_internal_launch_status();
+      return e == DPC_OK ? DPC_EHIP : e;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return DPC_OK;
+}
+
+}  // namespace
+
+extern "C" int dpc_nlist_build_noalloc(void* stream, int nloc, int ntypes, const int* sel,
+                                       double box, double rc, const double* coord,
+                                       const int* atype, int* nlist, int* status) {
+  NlGeo g;
+  const int st = make_geo(nloc, ntypes, sel, box, rc, &g);
+  if (st != DPC_OK) return st;
+  if (nloc > DPC_NLIST_NOALLOC_MAX_ATOMS || layout(nloc, g.ncell).total > kScratchBytes)
+    return DPC_ENOTSUP;
+  if (nloc == 0) return DPC_OK;
+  if (!coord || !atype || !nlist) return DPC_EINVAL;
+  // the array of the GPU the stream runs on, which must be the current one
+  int cur = -1;
+  hipDevice_t sdev = -1;
+  if (hipGetDevice(&cur) != hipSuccess ||
+      hipStreamGetDevice(static_cast<hipStream_t>(stream), &sdev) != hipSuccess) {
+    const int e = dpc_internal_launch_status();
+    return e == DPC_OK ? DPC_EHIP : e;
+  }
+  if (sdev != cur) return DPC_EINVAL;
+  void* ws = nullptr;
+  const int sa = scratch_address(cur, &ws);
+  if (sa != DPC_OK) return sa;
+  return dpc_nlist_launch(stream, nloc, ntypes, sel, box, rc, coord, atype, ws, kScratchBytes,
+                          nlist, status, nullptr);
+}
+
 extern "C" size_t dpc_nlist_workspace_bytes(int nloc, double box, double rc) {
   return dpc_nlist_scratch_bytes(nloc, box, rc);
 }
@@ -355,5 +423,5 @@ extern "C" int dpc_nlist_build(void* stream, int nloc, int ntypes, const int* se
                                double rc, const double* coord, const int* atype, void* workspace,
                                size_t workspace_bytes, int* nlist, int* status_host) {
   return dpc_nlist_launch(stream, nloc, ntypes, sel, box, rc, coord, atype, workspace,
-                          workspace_bytes, nlist, status_host);
+                          workspace_bytes, nlist, nullptr, status_host);
 }

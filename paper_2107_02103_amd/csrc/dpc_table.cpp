@@ -29,7 +29,7 @@ extern "C" const char* dpc_strerror(int status) {
     case DPC_EINVAL: return "invalid argument (null pointer, size, shape or dtype)";
     case DPC_ERANGE: return "invalid table range (stride <= 0, interval count < 1 or non-finite bound)";
     case DPC_EHIP: return "HIP runtime or kernel launch error";
-    case DPC_ENOTSUP: return "unsupported size (m1 > 256, more than 8 atom types, or more atoms within r_c than a list can hold)";
+    case DPC_ENOTSUP: return "unsupported size (m1 > 256, more than 8 atom types, more atoms within r_c than a list can hold, or more atoms than the no-allocation neighbour list holds)";
     case DPC_EOVERFLOW: return "neighbour list truncated: more atoms of some type within r_c than sel allows";
     default: return "unknown status";
   }
