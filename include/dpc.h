@@ -47,8 +47,10 @@ extern "C" {
 /* Arithmetic of the kernels.
  *  DPC_F64        float64 table, R~, dE/dT, T, D and dE/dR~.
  *  DPC_F32        float32 table, R~, dE/dT, T, D and dE/dR~, float32 arithmetic.
- *  DPC_F32_ACC64  float32 table, R~ and dE/dT; polynomial evaluated in float32,
- *                 T, D and dE/dR~ accumulated and stored in float64.          */
+ *  DPC_F32_ACC64  float32 table, R~ and dE/dT; in the forward the polynomial
+ *                 is evaluated in float32, T and D accumulated and stored in
+ *                 float64; the backward (m1 <= 128) converts its float32
+ *                 inputs to float64 and runs like DPC_F64, dE/dR~ in float64.  */
 typedef enum { DPC_F64 = 0, DPC_F32 = 1, DPC_F32_ACC64 = 2 } dpc_dtype;
 
 /* Tabulation range of one embedding net (one ordered type pair).
@@ -140,8 +142,9 @@ int dpc_se_a_tab_fwd(void* stream, dpc_dtype dtype, int nloc, int ntypes, const 
 /* Backward of T (forces need dE/dR~, paper Sec. II):
  *   dE/dR~_ij[k] = sum_m dE/dT_i[m][k] g_m(x) + (k == 0) sum_m g'_m(x) w_m,
  *   w_m = sum_k' dE/dT_i[m][k'] R~_ij[k'],  x = R~_ij[0],
- * for valid j; padded rows are written as 0.  For DPC_F64 with m1 <= 128 the
- * channel sums are formed per (interval, atom) pair on the matrix cores, as
+ * for valid j; padded rows are written as 0.  For DPC_F64 and DPC_F32_ACC64
+ * with m1 <= 128 the channel sums are formed per (interval, atom) pair on the
+ * matrix cores in float64, as
  * P[k][q] = sum_m dE/dT_i[m][k] C[m][q] followed by a polynomial in t per
  * neighbour: the same sums in another order of rounding.
  *   dE_dT    device [nloc][m1][4] (float64 for DPC_F64, else float32)

@@ -918,9 +918,12 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
 // row or past the interval, inside the slot.
 constexpr int kMfmaAtoms = 4;      // atoms per wavefront in the matrix-core kernel
 
-// 16-byte loads that copy one interval: its 48 ld bytes and the reads of the
-// last K step (up to channel 16 S - 1 of row 2) fit in NS KiB.
-__host__ __device__ constexpr int mfma_slot_kib(int S, int ld) { return (2 * ld + 16 * S + 63) / 64; }
+// 16-byte loads that copy one interval: its 6 ld elements and the reads of
+// the last K step (up to channel 16 S - 1 of row 2) fit in NS KiB; a power
+// pair of one channel is 2 esize bytes (16 for float64, 8 for float32).
+__host__ __device__ constexpr int mfma_slot_kib(int S, int ld, int esize = 8) {
+  return ((2 * ld + 16 * S) * 2 * esize + 1023) / 1024;
+}
 
 // The (interval, atom) products are stored as rows of 6 doubles, 26 doubles
 // (13 bank groups) apart, so that the records of up to 16 different products
@@ -1003,6 +1006,45 @@ __device__ __forceinline__ void lds_read_steps(uint32_t a, v4i (&q)[S]) {
 #undef DPC_R
 }
 
+// q[st] = 8 bytes at a + 128 st (S reads): float32 power pairs
+template <int S>
+__device__ __forceinline__ void lds_read_steps_b64(uint32_t a, v2i (&q)[S]) {
+  static_assert(S >= 1 && S <= 8, "K steps");
+#define DPC_R(i, off) "ds_read_b64 %" #i ", %[a] offset:" #off "\n\t"
+  if constexpr (S == 1)
+    asm volatile(DPC_R(0, 0) "s_waitcnt lgkmcnt(0)" : "=&v"(q[0]) : [a] "v"(a) : "memory");
+  else if constexpr (S == 2)
+    asm volatile(DPC_R(0, 0) DPC_R(1, 128) "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(q[0]), "=&v"(q[1]) : [a] "v"(a) : "memory");
+  else if constexpr (S == 3)
+    asm volatile(DPC_R(0, 0) DPC_R(1, 128) DPC_R(2, 256) "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(q[0]), "=&v"(q[1]), "=&v"(q[2]) : [a] "v"(a) : "memory");
+  else if constexpr (S == 4)
+    asm volatile(DPC_R(0, 0) DPC_R(1, 128) DPC_R(2, 256) DPC_R(3, 384) "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(q[0]), "=&v"(q[1]), "=&v"(q[2]), "=&v"(q[3]) : [a] "v"(a) : "memory");
+  else if constexpr (S == 5)
+    asm volatile(DPC_R(0, 0) DPC_R(1, 128) DPC_R(2, 256) DPC_R(3, 384) DPC_R(4, 512) "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(q[0]), "=&v"(q[1]), "=&v"(q[2]), "=&v"(q[3]), "=&v"(q[4])
+                 : [a] "v"(a) : "memory");
+  else if constexpr (S == 6)
+    asm volatile(DPC_R(0, 0) DPC_R(1, 128) DPC_R(2, 256) DPC_R(3, 384) DPC_R(4, 512) DPC_R(5, 640) "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(q[0]), "=&v"(q[1]), "=&v"(q[2]), "=&v"(q[3]), "=&v"(q[4]), "=&v"(q[5])
+                 : [a] "v"(a) : "memory");
+  else if constexpr (S == 7)
+    asm volatile(DPC_R(0, 0) DPC_R(1, 128) DPC_R(2, 256) DPC_R(3, 384) DPC_R(4, 512) DPC_R(5, 640) DPC_R(6, 768)
+                 "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(q[0]), "=&v"(q[1]), "=&v"(q[2]), "=&v"(q[3]), "=&v"(q[4]), "=&v"(q[5]),
+                   "=&v"(q[6])
+                 : [a] "v"(a) : "memory");
+  else
+    asm volatile(DPC_R(0, 0) DPC_R(1, 128) DPC_R(2, 256) DPC_R(3, 384) DPC_R(4, 512) DPC_R(5, 640) DPC_R(6, 768) DPC_R(7, 896)
+                 "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(q[0]), "=&v"(q[1]), "=&v"(q[2]), "=&v"(q[3]), "=&v"(q[4]), "=&v"(q[5]),
+                   "=&v"(q[6]), "=&v"(q[7])
+                 : [a] "v"(a) : "memory");
+#undef DPC_R
+}
+
 // Two rows (12 doubles) of a product at a (6 reads of 16 bytes).
 __device__ __forceinline__ void lds_read_rows2(uint32_t a, v4i (&q)[6]) {
   asm volatile(
@@ -1026,12 +1068,15 @@ __device__ __forceinline__ void wait_copies() {
 }
 
 // up to 128 channels: registers capped so that 3 wavefronts fit on a SIMD
-template <int S, int NS, bool kOne>
+// TI: storage of the table, R~ and dE/dT (float64, or float32 for the
+// mixed mode: converted to float64 as they are read); TO: dE/dR~.  The
+// products and the per-record polynomials are float64 in both.
+template <typename TI, typename TO, int S, int NS, bool kOne>
 __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(3)))
-void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
+void se_a_bwd_mfma_kernel(const Geo g, const TI* __restrict__ coeff,
                           const int* __restrict__ atype, const int* __restrict__ nlist,
-                          const double* __restrict__ em, const double* __restrict__ dT,
-                          double* __restrict__ dR) {
+                          const TI* __restrict__ em, const TI* __restrict__ dT,
+                          TO* __restrict__ dR) {
   static_assert(S >= 1 && S <= 8, "K steps per channel block");
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int NB = kMfmaAtoms;
@@ -1054,7 +1099,8 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
   // B column x of chain c is the power 2x + c, so that one 16-byte read of a
   // power pair gives a lane both chains' operands (x = 3 repeats the pair of
   // powers 4 and 5: those columns are not used)
-  const uint32_t bread = lds_addr(slot_p) + (uint32_t)(min(x, 2) * ld + 4 * kk + h) * 16u;
+  const uint32_t bread =
+      lds_addr(slot_p) + (uint32_t)(min(x, 2) * ld + 4 * kk + h) * (uint32_t)(2 * sizeof(TI));
   auto channel = [&](int s) __attribute__((always_inline)) { return 16 * s + 4 * kk + h; };
 
   // A operands: dT of the wave's atoms, transposed, zero past M1
@@ -1067,14 +1113,14 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
     for (int s = 0; s < S; ++s) {
       const int m = channel(s);
       A[a][s] = (i < g.nloc && m < m1)
-                    ? __builtin_nontemporal_load(dT + ((size_t)i * m1 + m) * 4 + x)
+                    ? (double)__builtin_nontemporal_load(dT + ((size_t)i * m1 + m) * 4 + x)
                     : 0.0;
     }
     ai[a] = -1;
     if (i < g.nloc) {
       const int t = __builtin_amdgcn_readfirstlane(atype[i]);
       if (t < 0 || t >= g.ntypes) {  // invalid type: the atom's outputs become NaN
-        for (int e = lane; e < nnei * 4; e += 64) dR[(size_t)i * nnei * 4 + e] = (double)NAN;
+        for (int e = lane; e < nnei * 4; e += 64) dR[(size_t)i * nnei * 4 + e] = (TO)NAN;
       } else {
         ai[a] = t;
       }
@@ -1085,7 +1131,7 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
   // the interval's offset goes into the range-checked vector offset, so
   // that the bytes read past the last interval of the buffer come back as 0
   auto fetch = [&](int off) __attribute__((always_inline)) {
-    const int voff = off * (int)sizeof(double) + lane * 16;
+    const int voff = off * (int)sizeof(TI) + lane * 16;
 #pragma unroll
     for (int i = 0; i < NS; ++i)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
@@ -1096,7 +1142,7 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
   const int nch = (nnei + kC - 1) / kC;
   int s0 = ((int)(blockIdx.x * 5 + wave * 3) % nch) * kC;
   uint32_t vm = 0, occ = 0;
-  double pre[4];      // R~ rows of chunk set pre_s0, loaded ahead (valid slots use them)
+  TI pre[4];          // R~ rows of chunk set pre_s0, loaded ahead (valid slots use them)
   int pre_s0 = -1;
   for (int cc = 0, wbase = -1; cc < nch; ++cc, s0 = s0 + kC < nnei ? s0 + kC : 0) {
     if (s0 - s0 % (kWindow / NB) != wbase) {  // window of nlist signs holding s0
@@ -1105,12 +1151,12 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
       occ = occupied_chunks<NB>(vm);
     }
     if (!((occ >> ((s0 - wbase) / kC)) & 1)) {   // padding only: zero rows
-      zero_rows<double, NB>(g, ai, i0, s0, dR, lane);
+      zero_rows<TO, NB>(g, ai, i0, s0, dR, lane);
       continue;
     }
     int pair;
-    Rec<double> mine;
-    const Tables tb = build_chunk_set<double, double, NB, true, kOne, true>(
+    Rec<TI> mine;
+    const Tables tb = build_chunk_set<TI, double, NB, true, kOne, true>(
         g, ai, i0, s0, wbase, vm, em, nullptr, W, lane, &pair, &mine, pre_s0 == s0, pre);
     // the rows of the next chunk set are loaded during this one's last run
     const int s0n = s0 + kC < nnei ? s0 + kC : 0;
@@ -1143,10 +1189,10 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
             der[k] = d;
           }
           // clamped records carry a zero row, which removes the derivative term
-          double o0 = fma(mine.r[0], der[0], val[0]);
-          o0 = fma(mine.r[1], der[1], o0);
-          o0 = fma(mine.r[2], der[2], o0);
-          out[0] = fma(mine.r[3], der[3], o0);
+          double o0 = fma((double)mine.r[0], der[0], val[0]);
+          o0 = fma((double)mine.r[1], der[1], o0);
+          o0 = fma((double)mine.r[2], der[2], o0);
+          out[0] = fma((double)mine.r[3], der[3], o0);
           out[1] = val[1];
           out[2] = val[2];
           out[3] = val[3];
@@ -1165,7 +1211,7 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
         constexpr bool kLast = decltype(last)::value;
         wait_copies();
         double Bc[2][S];
-        {
+        if constexpr (sizeof(TI) == 8) {
           v4i q[S];
           lds_read_steps<S>(bread, q);
 #pragma unroll
@@ -1173,6 +1219,15 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
             const Pair<double> v = __builtin_bit_cast(Pair<double>, q[st]);
             Bc[0][st] = v.x;
             Bc[1][st] = v.y;
+          }
+        } else {
+          v2i q[S];
+          lds_read_steps_b64<S>(bread, q);
+#pragma unroll
+          for (int st = 0; st < S; ++st) {
+            const Pair<float> v = __builtin_bit_cast(Pair<float>, q[st]);
+            Bc[0][st] = (double)v.x;
+            Bc[1][st] = (double)v.y;
           }
         }
         if constexpr (!kLast) {
@@ -1219,8 +1274,10 @@ void se_a_bwd_mfma_kernel(const Geo g, const double* __restrict__ coeff,
       run(tb.nruns - 1, std::true_type{});
     }
     // each lane writes the dE/dR~ row of its own slot (zero for padding)
-    if (tb.rank >= -1)
-      store_row(dR + ((size_t)(i0 + lane / kC) * nnei + s0 + lane % kC) * 4, out);
+    if (tb.rank >= -1) {
+      const TO o[4] = {(TO)out[0], (TO)out[1], (TO)out[2], (TO)out[3]};
+      store_row(dR + ((size_t)(i0 + lane / kC) * nnei + s0 + lane % kC) * 4, o);
+    }
     wave_sync();
   }
 }
@@ -1308,28 +1365,30 @@ int launch_fwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
   return launch_status();
 }
 
-// float64 with M1 <= 128: the matrix-core kernel, ceil(M1 / 16) K steps per
-// channel block, an interval copied by mfma_slot_kib(S, ld) loads (ld lies in
-// [16 S - 12, 16 S], so that count takes one of two values per S)
-template <int S>
+// M1 <= 128, float64 or mixed: the matrix-core kernel, ceil(M1 / 16) K steps
+// per channel block, an interval copied by mfma_slot_kib(S, ld, esize) loads
+// (ld lies in [16 S - 12, 16 S], so that count takes one of two values per S)
+template <typename TI, typename TO, int S>
 void launch_mfma_s(hipStream_t s, const Geo& g, dim3 grid, dim3 block, const void* coeff,
                    const int* atype, const int* nlist, const void* em, const void* dT, void* dR) {
-  const int ns = mfma_slot_kib(S, g.ld);
+  constexpr int es = (int)sizeof(TI);
+  const int ns = mfma_slot_kib(S, g.ld, es);
   auto go = [&](auto kern, size_t wave_bytes) {
-    hipLaunchKernelGGL(kern, grid, block, kWaves * wave_bytes, s, g, (const double*)coeff,
-                       atype, nlist, (const double*)em, (const double*)dT, (double*)dR);
+    hipLaunchKernelGGL(kern, grid, block, kWaves * wave_bytes, s, g, (const TI*)coeff, atype,
+                       nlist, (const TI*)em, (const TI*)dT, (TO*)dR);
   };
-  constexpr int lo = mfma_slot_kib(S, 16 * S - 12);
-  static_assert(mfma_slot_kib(S, 16 * S) <= lo + 1, "two slot sizes per S");
+  constexpr int lo = mfma_slot_kib(S, 16 * S - 12, es);
+  static_assert(mfma_slot_kib(S, 16 * S, es) <= lo + 1, "two slot sizes per S");
   if (g.ntypes == 1) {
-    if (ns <= lo) go(se_a_bwd_mfma_kernel<S, lo, true>, bwdm_wave_bytes(lo));
-    else go(se_a_bwd_mfma_kernel<S, lo + 1, true>, bwdm_wave_bytes(lo + 1));
+    if (ns <= lo) go(se_a_bwd_mfma_kernel<TI, TO, S, lo, true>, bwdm_wave_bytes(lo));
+    else go(se_a_bwd_mfma_kernel<TI, TO, S, lo + 1, true>, bwdm_wave_bytes(lo + 1));
   } else {
-    if (ns <= lo) go(se_a_bwd_mfma_kernel<S, lo, false>, bwdm_wave_bytes(lo));
-    else go(se_a_bwd_mfma_kernel<S, lo + 1, false>, bwdm_wave_bytes(lo + 1));
+    if (ns <= lo) go(se_a_bwd_mfma_kernel<TI, TO, S, lo, false>, bwdm_wave_bytes(lo));
+    else go(se_a_bwd_mfma_kernel<TI, TO, S, lo + 1, false>, bwdm_wave_bytes(lo + 1));
   }
 }
 
+template <typename TI, typename TO>
 int launch_bwd_mfma(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
                     const int* nlist, const void* em, const void* dT, void* dR) {
   const int S = (g.m1 + 15) / 16;
@@ -1337,14 +1396,14 @@ int launch_bwd_mfma(hipStream_t s, const Geo& g, const void* coeff, const int* a
   const dim3 grid((g.nloc + kWaves * NB - 1) / (kWaves * NB)), block(64 * kWaves);
   (void)hipGetLastError();  // report only what this launch raises
   switch (S) {
-    case 1: launch_mfma_s<1>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
-    case 2: launch_mfma_s<2>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
-    case 3: launch_mfma_s<3>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
-    case 4: launch_mfma_s<4>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
-    case 5: launch_mfma_s<5>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
-    case 6: launch_mfma_s<6>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
-    case 7: launch_mfma_s<7>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
-    default: launch_mfma_s<8>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
+    case 1: launch_mfma_s<TI, TO, 1>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
+    case 2: launch_mfma_s<TI, TO, 2>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
+    case 3: launch_mfma_s<TI, TO, 3>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
+    case 4: launch_mfma_s<TI, TO, 4>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
+    case 5: launch_mfma_s<TI, TO, 5>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
+    case 6: launch_mfma_s<TI, TO, 6>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
+    case 7: launch_mfma_s<TI, TO, 7>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
+    default: launch_mfma_s<TI, TO, 8>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
   }
   return launch_status();
 }
@@ -1352,11 +1411,11 @@ int launch_bwd_mfma(hipStream_t s, const Geo& g, const void* coeff, const int* a
 template <typename TI, typename TA>
 int launch_bwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype, const int* nlist,
                const void* em, const void* dT, void* dR) {
-#ifndef DPC_BWD_VALU_ONLY
-  if constexpr (sizeof(TI) == 8 && sizeof(TA) == 8) {
-    if (g.m1 <= 128) return launch_bwd_mfma(s, g, coeff, atype, nlist, em, dT, dR);
+  // float64 and the mixed mode (float64 accumulation) on the matrix cores;
+  // the float32 mode keeps float32 arithmetic on the vector ALUs
+  if constexpr (sizeof(TA) == 8) {
+    if (g.m1 <= 128) return launch_bwd_mfma<TI, TA>(s, g, coeff, atype, nlist, em, dT, dR);
   }
-#endif
   constexpr int NB = DPC_BWD_ATOMS_PER_WAVE;
   static_assert(NB == 1 || NB == 2 || NB == 4 || NB == 8, "atoms per wave: 1, 2, 4 or 8");
   const dim3 grid((g.nloc + kWaves * NB - 1) / (kWaves * NB)), block(64 * kWaves);

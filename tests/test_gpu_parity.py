@@ -179,6 +179,20 @@ def test_edge_shapes_and_ranges(sel, m1, m2):
     assert np.all(got[0][5] == 0) and np.all(got[1][5] == 0) and np.all(got[2][5] == 0)
 
 
+@pytest.mark.parametrize("dtype", ["f32acc64", "f32"])
+@pytest.mark.parametrize("sel,m1,m2", [((3, 70), 100, 16), ((77,), 17, 4), ((40, 33), 128, 16),
+                                       ((20,), 113, 16), ((50,), 129, 8), ((700, 900), 100, 16)])
+def test_edge_shapes_float32_modes(sel, m1, m2, dtype):
+    # the mixed mode's backward on the matrix cores (float32 tables copied
+    # into LDS, 8 bytes per power pair) and the float32 vector kernels
+    x = _synthetic(37, sel, m1, m2, seed=sum(sel) + m1 + 7)
+    x.nlist[5] = -1
+    x.em[5] = 0
+    _, _, out = _run_gpu(x, dtype)
+    got = tuple(t.cpu().numpy().astype(np.float64) for t in out)
+    _check(x, np.arange(37), got, dtype)
+
+
 def test_empty_and_single_atom():
     import paper_2107_02103_amd as P
     x = _synthetic(1, (40,), 100, 16, seed=3)
