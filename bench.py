@@ -339,8 +339,11 @@ def bench_fitting(args):
 def bench_chain(args):
     """Positions to energies and forces: dpc_env_mat_a (R~), dpc_se_a_tab_fwd
     (T, D), dpc_fitting_fwd_bwd (E, dE/dD; seeded random fitting net),
-    dpc_descriptor_bwd (dE/dT), dpc_se_a_tab_bwd (dE/dR~) and dpc_force_a,
-    one call each per step on one stream, the reverse slots built once.
+    dpc_se_a_tab_bwd_from_dD (dE/dT formed inside the backward, then dE/dR~)
+    and dpc_force_a, one call each per step on one stream.  The neighbour
+    list (dpc_nlist_build) and its reverse slots are built once from the
+    positions, as an MD code does every few steps; the descriptor backward
+    and the backward as two calls are timed once beside the fused call.
     float64."""
     import numpy as np
     import torch
@@ -358,7 +361,9 @@ def bench_chain(args):
     op = P.SeATab(x.nets, x.lo, x.L1, x.L2, cfg.d1, cfg.d2, cfg.sel, m2)
     coord = torch.from_numpy(x.coords).cuda()
     at = torch.from_numpy(x.atype).cuda()
-    nl = torch.from_numpy(x.nlist).cuda()
+    nl = torch.empty((n, nnei), dtype=torch.int32, device="cuda")
+    nlb = P.dpc_nlist_workspace_bytes(n, cfg.box, cfg.rc)
+    nlws = torch.empty(nlb, dtype=torch.uint8, device="cuda")
     fnet, keep, ws, nb, hblas = _fitting_setup(n, m1, m2)
     Ea = torch.empty(n, dtype=torch.float64, device="cuda")
     dD = torch.empty((n, m1, m2), dtype=torch.float64, device="cuda")
@@ -371,7 +376,7 @@ def bench_chain(args):
     F = torch.empty((n, 3), dtype=torch.float64, device="cuda")
     V = torch.empty((n, 9), dtype=torch.float64, device="cuda")
     s = torch.cuda.Stream()
-    names = ["env", "fwd", "fitting", "descriptor_bwd", "bwd", "force"]
+    names = ["env", "fwd", "fitting", "bwd_from_dD", "force"]
 
     def step(evs=None):
         calls = [
@@ -379,8 +384,7 @@ def bench_chain(args):
                                     st["sigma"], st["sigma_all"], coord, at, nl, em),
             lambda: op.forward(em, nl, at, T, D, stream=s),
             lambda: P.dpc_fitting_fwd_bwd(s, hblas.value, n, fnet, D, ws, nb, Ea, dD),
-            lambda: op.descriptor_backward(T, dD, dT, stream=s),
-            lambda: op.backward(em, nl, at, dT, dR, stream=s),
+            lambda: op.backward_from_dD(em, nl, at, T, dD, dR, stream=s),
             lambda: P.dpc_force_a(s, P.DPC_F64, n, cfg.ntypes, nnei, cfg.box, cfg.rc, cfg.rcs, st["sigma"],
                                   st["sigma_all"], coord, at, nl, rev, dR, F, V),
         ]
@@ -391,11 +395,33 @@ def bench_chain(args):
         if evs is not None:
             evs[-1].record(s)
 
+    once = {}
     with torch.cuda.stream(s):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev[0].record(s)
+        P.dpc_nlist_build(s, n, cfg.ntypes, cfg.sel, cfg.box, cfg.rc, coord, at, nlws, nlb, nl, wait=False)
+        ev[1].record(s)
         P.dpc_nlist_reverse(s, n, cfg.ntypes, cfg.sel, cfg.box, coord, at, nl, rev)
+        ev[2].record(s)
+        torch.cuda.synchronize()
+        status = nlws[:8].view(torch.int32).cpu().tolist()
+        if status != [0, 0]:
+            raise RuntimeError(f"neighbour list status {status} (truncated, over capacity)")
+        once["nlist"] = ev[0].elapsed_time(ev[1])
+        once["reverse"] = ev[1].elapsed_time(ev[2])
         for _ in range(args.warmup):
             step()
         torch.cuda.synchronize()
+        # the same backward as two calls, for comparison
+        ev2 = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev2[0].record(s)
+        op.descriptor_backward(T, dD, dT, stream=s)
+        ev2[1].record(s)
+        op.backward(em, nl, at, dT, dR, stream=s)
+        ev2[2].record(s)
+        torch.cuda.synchronize()
+        once["descriptor_bwd (two-call path)"] = ev2[0].elapsed_time(ev2[1])
+        once["bwd (two-call path)"] = ev2[1].elapsed_time(ev2[2])
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(args.steps)]
         t0 = time.perf_counter()
         for e in evs:
@@ -410,8 +436,69 @@ def bench_chain(args):
         "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
         "config": {"workload": f"{cfg.name}: {n} atoms, sel {list(cfg.sel)}; random fitting net 240-240-240",
                    "atoms": n, "valid_pairs": pairs},
-        "kernel_ms": per,
+        "kernel_ms": per, "once_ms": once, "library": library_record(),
     }
+    print(json.dumps(res), flush=True)
+
+
+def bench_nlist(args):
+    """dpc_nlist_build over the configuration's positions (cell list, then one
+    wavefront per atom ranking its candidates).  Algorithmic bytes: the
+    positions and types in (28 B per atom) and the list out (4 B per slot)."""
+    import numpy as np
+    import torch
+    import paper_2107_02103_amd as P
+    from synth import make_inputs
+    from synth.configs import get_config
+    key = int(args.config) if args.config.isdigit() else args.config
+    cfg = get_config(key)
+    log(f"[bench] neighbour list: generating {cfg.name}")
+    x = make_inputs(cfg, with_grad=False)
+    n, nnei = cfg.natoms, cfg.nnei
+    coord = torch.from_numpy(x.coords).cuda()
+    at = torch.from_numpy(x.atype).cuda()
+    nl = torch.empty((n, nnei), dtype=torch.int32, device="cuda")
+    nb = P.dpc_nlist_workspace_bytes(n, cfg.box, cfg.rc)
+    ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+    s = torch.cuda.Stream()
+    run = lambda: P.dpc_nlist_build(s, n, cfg.ntypes, cfg.sel, cfg.box, cfg.rc, coord, at, ws, nb, nl,
+                                    wait=False)
+    with torch.cuda.stream(s):
+        for _ in range(args.warmup):
+            run()
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        t0 = time.perf_counter()
+        for a, b in evs:
+            a.record(s); run(); b.record(s)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+    ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    same = bool(np.array_equal(nl.cpu().numpy(), x.nlist))
+    nbytes = 28.0 * n + 4.0 * n * nnei
+    achieved = nbytes / (ms * 1e-3) / 1e9
+    res = {"metric": "neighbour list build (cell list, type-then-distance order), atoms/s",
+           "value": n * args.steps / wall, "unit": "atoms/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": wall / args.steps * 1e3, "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+           "config": {"workload": f"{cfg.name}: {n} atoms, box {cfg.box:.3f}, rc {cfg.rc}, sel {list(cfg.sel)}",
+                      "atoms": n, "workspace_bytes": nb},
+           "ms": ms, "equals_generator_lists": same,
+           "roofline": roofline_entry("hbm", "nl_list_kernel", achieved, 8000.0, "GB/s", cfg.name),
+           "library": library_record()}
+    if not args.no_cpu_baseline:
+        from oracle import nlist as onl
+        t0, done, chunk = time.perf_counter(), 0, 64
+        while done < n and time.perf_counter() - t0 < args.cpu_seconds:
+            onl.neighbour_list(x.coords, x.atype, cfg.sel, cfg.box, cfg.rc,
+                               centres=np.arange(done, min(n, done + chunk)))
+            done = min(n, done + chunk)
+        dt = time.perf_counter() - t0
+        from oracle import cref
+        res["cpu_baseline"] = {"value": done / dt, "unit": "atoms/s", "cores": cref.num_threads(),
+                               "kind": "oracle", "sample": f"atoms 0..{done - 1} of {n} (brute force "
+                               f"over all atoms), {dt:.1f} s"}
     print(json.dumps(res), flush=True)
 
 
@@ -430,6 +517,7 @@ def main():
     ap.add_argument("--chain", action="store_true",
                     help="time positions -> R~ -> T, D -> E, dE/dD -> dE/dT -> dE/dR~ -> forces")
     ap.add_argument("--fitting", action="store_true", help="time the fitting net (energy and dE/dD)")
+    ap.add_argument("--nlist", action="store_true", help="time the neighbour-list build")
     ap.add_argument("--env-force", action="store_true",
                     help="time the environment matrix and the force / virial assembly instead")
     ap.add_argument("--descriptor-bwd", action="store_true",
@@ -461,6 +549,9 @@ def main():
         return
     if args.fitting:
         bench_fitting(args)
+        return
+    if args.nlist:
+        bench_nlist(args)
         return
 
     import numpy as np

@@ -155,6 +155,24 @@ int dpc_se_a_tab_bwd(void* stream, dpc_dtype dtype, int nloc, int ntypes, const 
                      const int* atype, const int* nlist, const void* em,
                      const void* dE_dT, void* dE_dem);
 
+/* The backward from dE/dD: dpc_descriptor_bwd fused into dpc_se_a_tab_bwd.
+ * The matrix-core backward forms dE/dT of its atoms itself, in a prologue on
+ * the matrix cores,
+ * from the forward's T and dE/dD (paper Sec. II: D_i = T_i (T_i<)^T), so dE/dT
+ * is never stored:
+ *   dE/dT_i[m][k] = sum_{n<m2} dE/dD_i[m][n] T_i[n][k] + (m < m2) sum_{m'} dE/dD_i[m'][m] T_i[m'][k],
+ * then dE/dR~ as dpc_se_a_tab_bwd.  The result equals the two calls up to the
+ * order of rounding.
+ *   T       device float64 [nloc][m1][4] (the forward's T), 16-byte aligned
+ *   dE_dD   device float64 [nloc][m1][m2], 16-byte aligned
+ *   dE_dem  device out float64 [nloc][nnei][4], 16-byte aligned
+ * Requires DPC_F64, m1 <= 128 and an even m2 <= 16 (DPC_ENOTSUP otherwise:
+ * use the two calls).  Other arguments as dpc_se_a_tab_bwd.                 */
+int dpc_se_a_tab_bwd_from_dD(void* stream, dpc_dtype dtype, int nloc, int ntypes, const int* sel,
+                             int m1, int m2, const dpc_range* ranges, const void* coeff,
+                             const int* atype, const int* nlist, const void* em, const void* T,
+                             const void* dE_dD, void* dE_dem);
+
 /* Backward of the descriptor (paper Sec. II: D_i = T_i (T_i<)^T, T_i< the
  * first m2 rows of T_i, i.e. D_i[m][n] = sum_k T_i[m][k] T_i[n][k], n < m2):
  *   dE/dT_i[m][k] = sum_{n<m2} dE/dD_i[m][n] T_i[n][k]

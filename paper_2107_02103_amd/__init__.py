@@ -10,7 +10,7 @@ _BINDING = ("DPC_F32", "DPC_F32_ACC64", "DPC_F64", "DPC_OK", "DPC_EINVAL", "DPC_
             "dpc_descriptor_bwd", "dpc_env_mat_a", "dpc_fitting_fwd_bwd", "dpc_fitting_net",
             "dpc_fitting_workspace_bytes", "dpc_force_a", "dpc_last_hip_error", "RocblasHandle",
             "dpc_nlist_reverse", "dpc_nlist_workspace_bytes", "dpc_nlist_build",
-            "dpc_nlist_build_noalloc", "dpc_se_a_tab_bwd", "dpc_se_a_tab_fwd", "dpc_strerror",
+            "dpc_nlist_build_noalloc", "dpc_se_a_tab_bwd", "dpc_se_a_tab_bwd_from_dD", "dpc_se_a_tab_fwd", "dpc_strerror",
             "dpc_table_layout", "dpc_version", "make_ranges")
 
 

@@ -34,7 +34,8 @@ DPC_NLIST_NOALLOC_MAX_ATOMS = 524288
 EXPORTED = ("dpc_strerror", "dpc_last_hip_error", "dpc_version", "dpc_table_layout", "dpc_build_table",
             "dpc_se_a_tab_fwd", "dpc_se_a_tab_bwd", "dpc_descriptor_bwd", "dpc_env_mat_a",
             "dpc_nlist_reverse", "dpc_force_a", "dpc_fitting_workspace_bytes", "dpc_fitting_fwd_bwd",
-            "dpc_nlist_workspace_bytes", "dpc_nlist_build", "dpc_nlist_build_noalloc")
+            "dpc_nlist_workspace_bytes", "dpc_nlist_build", "dpc_nlist_build_noalloc",
+            "dpc_se_a_tab_bwd_from_dD")
 
 
 class dpc_range(C.Structure):
@@ -64,6 +65,12 @@ _lib.dpc_se_a_tab_bwd.restype = C.c_int
 _lib.dpc_se_a_tab_bwd.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.POINTER(C.c_int),
                                   C.c_int, C.POINTER(dpc_range), C.c_void_p, C.c_void_p,
                                   C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+_lib.dpc_se_a_tab_bwd_from_dD.restype = C.c_int
+_lib.dpc_se_a_tab_bwd_from_dD.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.POINTER(C.c_int),
+                                          C.c_int, C.c_int, C.POINTER(dpc_range), C.c_void_p, C.c_void_p,
+                                          C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+
+
 class dpc_fitting_net(C.Structure):
     _fields_ = [("n_in", C.c_int), ("width", C.c_int), ("W", C.c_void_p * 3), ("b", C.c_void_p * 3),
                 ("w_out", C.c_void_p), ("b_out", C.c_double)]
@@ -280,6 +287,21 @@ def dpc_se_a_tab_bwd(stream, dtype, nloc, ntypes, sel, m1, ranges, coeff, atype,
                                  _ptr(em, name="em"), _ptr(dE_dT, name="dE_dT"),
                                  _ptr(dE_dem, name="dE_dem")),
            "dpc_se_a_tab_bwd")
+
+
+def dpc_se_a_tab_bwd_from_dD(stream, dtype, nloc, ntypes, sel, m1, m2, ranges, coeff, atype, nlist,
+                             em, T, dE_dD, dE_dem):
+    nnei = sum(int(v) for v in sel)
+    _need(atype, nloc, 4, "atype"); _need(nlist, nloc * nnei, 4, "nlist")
+    _need(em, nloc * nnei * 4, 8, "em"); _need(T, nloc * m1 * 4, 8, "T")
+    _need(dE_dD, nloc * m1 * m2, 8, "dE_dD"); _need(dE_dem, nloc * nnei * 4, 8, "dE_dem")
+    _one_device(stream, coeff=coeff, atype=atype, nlist=nlist, em=em, T=T, dE_dD=dE_dD, dE_dem=dE_dem)
+    _check(_lib.dpc_se_a_tab_bwd_from_dD(_stream(stream), int(dtype), int(nloc), int(ntypes), _sel(sel),
+                                         int(m1), int(m2), ranges, _ptr(coeff, name="coeff"),
+                                         _ptr(atype, name="atype"), _ptr(nlist, name="nlist"),
+                                         _ptr(em, name="em"), _ptr(T, name="T"), _ptr(dE_dD, name="dE_dD"),
+                                         _ptr(dE_dem, name="dE_dem")),
+           "dpc_se_a_tab_bwd_from_dD")
 
 
 def dpc_descriptor_bwd(stream, dtype, nloc, m1, m2, T, dE_dD, dE_dT):

@@ -1068,15 +1068,86 @@ __device__ __forceinline__ void wait_copies() {
 }
 
 // up to 128 channels: registers capped so that 3 wavefronts fit on a SIMD
+// The A operands of the wavefront's NB atoms from T and dE/dD (the
+// descriptor backward), on the matrix cores.  Both sums are 4 x 4 x 4
+// products whose output layout is the A operand layout itself: output lane
+// L = 16 i + 4 b + j of block b holds channel 16 s + 4 i + b, column j, which
+// is where the A operand of K step s wants dE/dT[16 s + (L >> 2)][L & 3].
+//   first sum,  K = n < M':   A_b[x][kk] = dE/dD[16 s + 4 x + b][n(kk)],  B_b[kk][x] = T[n(kk)][x]
+//   second sum, K = m' < M1:  A_b[x][kk] = dE/dD[m'(kk)][4 x + b],        B_b[kk][x] = T[m'(kk)][x]
+// (the second only into step s = 0, output channels 4 x + b < M' <= 16).  In
+// the first sum the K steps come in pairs n = 8 q + 2 kk + {0, 1}, so one
+// 16-byte load gives a lane the A operands of two steps.  Operands outside
+// M1, M' are zero (loads clamped inside the atom's rows); atoms past nloc
+// get zeros.  T and dE/dD are read straight from memory (the second sum
+// re-reads dE/dD rows the first sum has just brought into the caches).
+template <int NB, int S>
+__device__ __forceinline__ void descriptor_bwd_operands(const Geo& g, int i0,
+                                                        const double* __restrict__ Tin,
+                                                        const double* __restrict__ dD, int lane,
+                                                        double (&A)[NB][S]) {
+  typedef double D2 __attribute__((ext_vector_type(2)));
+  const int m1 = g.m1, m2 = g.m2;
+  const int kk = lane >> 4, b = (lane >> 2) & 3, x = lane & 3;
+  const int nq = (m2 + 7) >> 3;           // 16-byte K pairs of the first sum (M' <= 16: 1 or 2)
+  const int np = (m1 + 3) >> 2;           // K steps of the second sum
+  const int col = 4 * x + b;              // second sum: the output channel of the lane's A row
+#pragma unroll
+  for (int a = 0; a < NB; ++a) {
+    const bool live = i0 + a < g.nloc;
+    const int i = min(i0 + a, g.nloc - 1);
+    const double* Ta = Tin + (size_t)i * m1 * 4;
+    const double* Da = dD + (size_t)i * m1 * m2;
+    double acc[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s) acc[s] = 0.0;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      if (q >= nq) break;
+      const int n = 8 * q + 2 * kk;
+      const bool nv = n < m2;             // m2 even: n + 1 < m2 too
+      const int nc = nv ? n : 0;
+      const double b0 = nv ? Ta[nc * 4 + x] : 0.0, b1 = nv ? Ta[nc * 4 + 4 + x] : 0.0;
+#pragma unroll
+      for (int s = 0; s < S; ++s) {
+        const int m = 16 * s + 4 * x + b;
+        const bool ok = nv && m < m1;
+        const D2 v = *reinterpret_cast<const D2*>(Da + (size_t)min(m, m1 - 1) * m2 + nc);
+        acc[s] = mfma4(ok ? v.x : 0.0, b0, acc[s]);
+        acc[s] = mfma4(ok ? v.y : 0.0, b1, acc[s]);
+      }
+    }
+    const bool cv = col < m2;
+    const int cc = cv ? col : 0;
+#pragma unroll 4
+    for (int p = 0; p < np; ++p) {
+      const int mp = 4 * p + kk;
+      const bool ok = mp < m1;
+      const int mc = ok ? mp : 0;
+      const double bt = ok ? Ta[mc * 4 + x] : 0.0;
+      const double at = ok && cv ? __builtin_nontemporal_load(Da + (size_t)mc * m2 + cc) : 0.0;
+      acc[0] = mfma4(at, bt, acc[0]);
+    }
+#pragma unroll
+    for (int s = 0; s < S; ++s) A[a][s] = live && 16 * s + (lane >> 2) < m1 ? acc[s] : 0.0;
+  }
+}
+
 // TI: storage of the table, R~ and dE/dT (float64, or float32 for the
 // mixed mode: converted to float64 as they are read); TO: dE/dR~.  The
 // products and the per-record polynomials are float64 in both.
-template <typename TI, typename TO, int S, int NS, bool kOne>
+// kFromD: dE/dT is not an input but formed in a prologue from the forward's
+// T and dE/dD (float64, M' <= 16): the descriptor backward of D = T (T<)^T,
+//   dE/dT[m][k] = sum_{n<M'} dE/dD[m][n] T[n][k] + (m < M') sum_m' dE/dD[m'][m] T[m'][k],
+// evaluated per atom on the matrix cores straight into the A operands, so
+// dE/dT never goes to memory.
+template <typename TI, typename TO, int S, int NS, bool kOne, bool kFromD = false>
 __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(3)))
 void se_a_bwd_mfma_kernel(const Geo g, const TI* __restrict__ coeff,
                           const int* __restrict__ atype, const int* __restrict__ nlist,
                           const TI* __restrict__ em, const TI* __restrict__ dT,
-                          TO* __restrict__ dR) {
+                          TO* __restrict__ dR, const double* __restrict__ Tin = nullptr,
+                          const double* __restrict__ dD = nullptr) {
   static_assert(S >= 1 && S <= 8, "K steps per channel block");
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int NB = kMfmaAtoms;
@@ -1106,15 +1177,18 @@ void se_a_bwd_mfma_kernel(const Geo g, const TI* __restrict__ coeff,
   // A operands: dT of the wave's atoms, transposed, zero past M1
   double A[NB][S];
   int ai[NB];
+  if constexpr (kFromD) descriptor_bwd_operands<NB, S>(g, i0, Tin, dD, lane, A);
 #pragma unroll
   for (int a = 0; a < NB; ++a) {
     const int i = i0 + a;
+    if constexpr (!kFromD) {
 #pragma unroll
-    for (int s = 0; s < S; ++s) {
-      const int m = channel(s);
-      A[a][s] = (i < g.nloc && m < m1)
-                    ? (double)__builtin_nontemporal_load(dT + ((size_t)i * m1 + m) * 4 + x)
-                    : 0.0;
+      for (int s = 0; s < S; ++s) {
+        const int m = channel(s);
+        A[a][s] = (i < g.nloc && m < m1)
+                      ? (double)__builtin_nontemporal_load(dT + ((size_t)i * m1 + m) * 4 + x)
+                      : 0.0;
+      }
     }
     ai[a] = -1;
     if (i < g.nloc) {
@@ -1368,42 +1442,43 @@ int launch_fwd(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
 // M1 <= 128, float64 or mixed: the matrix-core kernel, ceil(M1 / 16) K steps
 // per channel block, an interval copied by mfma_slot_kib(S, ld, esize) loads
 // (ld lies in [16 S - 12, 16 S], so that count takes one of two values per S)
-template <typename TI, typename TO, int S>
+template <typename TI, typename TO, int S, bool kFromD>
 void launch_mfma_s(hipStream_t s, const Geo& g, dim3 grid, dim3 block, const void* coeff,
-                   const int* atype, const int* nlist, const void* em, const void* dT, void* dR) {
+                   const int* atype, const int* nlist, const void* em, const void* dT, void* dR,
+                   const double* Tin, const double* dD) {
   constexpr int es = (int)sizeof(TI);
   const int ns = mfma_slot_kib(S, g.ld, es);
   auto go = [&](auto kern, size_t wave_bytes) {
     hipLaunchKernelGGL(kern, grid, block, kWaves * wave_bytes, s, g, (const TI*)coeff, atype,
-                       nlist, (const TI*)em, (const TI*)dT, (TO*)dR);
+                       nlist, (const TI*)em, (const TI*)dT, (TO*)dR, Tin, dD);
   };
   constexpr int lo = mfma_slot_kib(S, 16 * S - 12, es);
   static_assert(mfma_slot_kib(S, 16 * S, es) <= lo + 1, "two slot sizes per S");
   if (g.ntypes == 1) {
-    if (ns <= lo) go(se_a_bwd_mfma_kernel<TI, TO, S, lo, true>, bwdm_wave_bytes(lo));
-    else go(se_a_bwd_mfma_kernel<TI, TO, S, lo + 1, true>, bwdm_wave_bytes(lo + 1));
+    if (ns <= lo) go(se_a_bwd_mfma_kernel<TI, TO, S, lo, true, kFromD>, bwdm_wave_bytes(lo));
+    else go(se_a_bwd_mfma_kernel<TI, TO, S, lo + 1, true, kFromD>, bwdm_wave_bytes(lo + 1));
   } else {
-    if (ns <= lo) go(se_a_bwd_mfma_kernel<TI, TO, S, lo, false>, bwdm_wave_bytes(lo));
-    else go(se_a_bwd_mfma_kernel<TI, TO, S, lo + 1, false>, bwdm_wave_bytes(lo + 1));
+    if (ns <= lo) go(se_a_bwd_mfma_kernel<TI, TO, S, lo, false, kFromD>, bwdm_wave_bytes(lo));
+    else go(se_a_bwd_mfma_kernel<TI, TO, S, lo + 1, false, kFromD>, bwdm_wave_bytes(lo + 1));
   }
 }
 
-template <typename TI, typename TO>
+template <typename TI, typename TO, bool kFromD = false>
 int launch_bwd_mfma(hipStream_t s, const Geo& g, const void* coeff, const int* atype,
-                    const int* nlist, const void* em, const void* dT, void* dR) {
+                    const int* nlist, const void* em, const void* dT, void* dR,
+                    const double* Tin = nullptr, const double* dD = nullptr) {
   const int S = (g.m1 + 15) / 16;
   constexpr int NB = kMfmaAtoms;
   const dim3 grid((g.nloc + kWaves * NB - 1) / (kWaves * NB)), block(64 * kWaves);
   (void)hipGetLastError();  // report only what this launch raises
   switch (S) {
-    case 1: launch_mfma_s<TI, TO, 1>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
-    case 2: launch_mfma_s<TI, TO, 2>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
-    case 3: launch_mfma_s<TI, TO, 3>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
-    case 4: launch_mfma_s<TI, TO, 4>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
-    case 5: launch_mfma_s<TI, TO, 5>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
-    case 6: launch_mfma_s<TI, TO, 6>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
-    case 7: launch_mfma_s<TI, TO, 7>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
-    default: launch_mfma_s<TI, TO, 8>(s, g, grid, block, coeff, atype, nlist, em, dT, dR); break;
+#define DPC_CASE(n)                                                                                \
+  case n:                                                                                          \
+    launch_mfma_s<TI, TO, n, kFromD>(s, g, grid, block, coeff, atype, nlist, em, dT, dR, Tin, dD); \
+    break;
+    DPC_CASE(1) DPC_CASE(2) DPC_CASE(3) DPC_CASE(4) DPC_CASE(5) DPC_CASE(6) DPC_CASE(7)
+#undef DPC_CASE
+    default: launch_mfma_s<TI, TO, 8, kFromD>(s, g, grid, block, coeff, atype, nlist, em, dT, dR, Tin, dD); break;
   }
   return launch_status();
 }
@@ -1460,6 +1535,28 @@ extern "C" int dpc_se_a_tab_fwd(void* stream, dpc_dtype dtype, int nloc, int nty
     case DPC_F32: return launch_fwd<float, float>(s, g, coeff, atype, nlist, em, T, D);
     default: return launch_fwd<float, double>(s, g, coeff, atype, nlist, em, T, D);
   }
+}
+
+extern "C" int dpc_se_a_tab_bwd_from_dD(void* stream, dpc_dtype dtype, int nloc, int ntypes,
+                                        const int* sel, int m1, int m2, const dpc_range* ranges,
+                                        const void* coeff, const int* atype, const int* nlist,
+                                        const void* em, const void* T, const void* dE_dD,
+                                        void* dE_dem) {
+  if (!dtype_ok(dtype)) return DPC_EINVAL;
+  Geo g;
+  const int st = make_geo(nloc, ntypes, sel, m1, m2, ranges, dtype == DPC_F64 ? 8 : 4, &g);
+  if (st != DPC_OK) return st;
+  // float64, the matrix-core backward (M1 <= 128), M' even and at most 16
+  if (dtype != DPC_F64 || m1 > 128 || m2 > 16 || m2 % 2) return DPC_ENOTSUP;
+  if (nloc == 0) return DPC_OK;
+  if (!coeff || !atype || !nlist || !em || !T || !dE_dD || !dE_dem) return DPC_EINVAL;
+  // rows of R~, dE/dR~, T and dE/dD are moved 16 bytes at a time
+  if (reinterpret_cast<uintptr_t>(em) % 16 || reinterpret_cast<uintptr_t>(dE_dem) % 16 ||
+      reinterpret_cast<uintptr_t>(T) % 16 || reinterpret_cast<uintptr_t>(dE_dD) % 16)
+    return DPC_EINVAL;
+  return launch_bwd_mfma<double, double, true>(static_cast<hipStream_t>(stream), g, coeff, atype,
+                                               nlist, em, nullptr, dE_dem, (const double*)T,
+                                               (const double*)dE_dD);
 }
 
 extern "C" int dpc_se_a_tab_bwd(void* stream, dpc_dtype dtype, int nloc, int ntypes,

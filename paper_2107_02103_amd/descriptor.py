@@ -57,6 +57,22 @@ class SeATab:
                            self.sel, self.m1, self.ranges, self.coeff, atype, nlist, em, dT, dR)
         return dR
 
+    def backward_from_dD(self, em, nlist, atype, T, dD, dR=None, stream=None):
+        """dE/dR~ from dE/dD and the forward's T in one call (the descriptor
+        backward fused into the backward; float64, M1 <= 128, even M' <= 16)."""
+        nloc = nlist.shape[0]
+        if dR is None:
+            dR = torch.empty((nloc, self.nnei, 4), dtype=self.t_acc, device=self.device)
+        self._check(em, nlist, atype)
+        if T.dtype != torch.float64 or tuple(T.shape) != (nloc, self.m1, 4):
+            raise ValueError("T has the wrong dtype or shape")
+        if dD.dtype != torch.float64 or tuple(dD.shape) != (nloc, self.m1, self.m2):
+            raise ValueError("dE/dD has the wrong dtype or shape")
+        B.dpc_se_a_tab_bwd_from_dD(stream or torch.cuda.current_stream(), self.dtype, nloc, self.ntypes,
+                                   self.sel, self.m1, self.m2, self.ranges, self.coeff, atype, nlist, em,
+                                   T, dD, dR)
+        return dR
+
     def descriptor_backward(self, T, dD, dT=None, stream=None):
         """dE/dT from dE/dD and the forward's T (the input dtype of backward())."""
         nloc = T.shape[0]
