@@ -617,12 +617,15 @@ def main():
     step_s = wall / args.steps
     peak = PEAK_TFLOPS[dtype]
     tflops = (flop_fwd + flop_bwd) / step_s / 1e12
-    # float64 backward passes with M1 <= 128 run on the matrix-core kernel (the
-    # library's rule); both FP64 peaks of MI355X, vector and matrix, are 78.6 TFLOP/s
-    bwd_mfma = dtype == "f64" and cfg.widths[-1] <= 128
+    # backward passes that accumulate in float64 (float64 and the mixed mode)
+    # with M1 <= 128 run on the matrix-core kernel (the library's rule), in
+    # float64 MFMA: its peak is the FP64 matrix peak, 78.6 TFLOP/s, as the
+    # FP64 vector peak
+    bwd_mfma = dtype in ("f64", "f32acc64") and cfg.widths[-1] <= 128
     bwd_name = "se_a_bwd_mfma_kernel" if bwd_mfma else "se_a_bwd_kernel"
     dom = bwd_name if bwd_ms >= fwd_ms else "se_a_fwd_kernel"
     bound = "mfma" if dom == "se_a_bwd_mfma_kernel" else "alu"
+    dom_peak = PEAK_TFLOPS["f64"] if bound == "mfma" else peak
     dom_ms = max(bwd_ms, fwd_ms)
     dom_flop = flop_bwd if bwd_ms >= fwd_ms else flop_fwd
     achieved = dom_flop / (dom_ms * 1e-3) / 1e12
@@ -650,7 +653,7 @@ def main():
         "frac_vector_peak": tflops / peak,
         "fwd_ms": fwd_ms,
         "bwd_ms": bwd_ms,
-        "roofline": roofline_entry(bound, dom, achieved, peak, "TFLOP/s", cfg.name, dtype,
+        "roofline": roofline_entry(bound, dom, achieved, dom_peak, "TFLOP/s", cfg.name, dtype,
                                    stored=not (args.stride or args.shard > 1)),
         "library": library_record(),
     }
