@@ -1234,7 +1234,9 @@ void se_a_bwd_mfma_kernel(const Geo g, const TI* __restrict__ coeff,
         g, ai, i0, s0, wbase, vm, em, nullptr, W, lane, &pair, &mine, pre_s0 == s0, pre);
     // the rows of the next chunk set are loaded during this one's last run
     const int s0n = s0 + kC < nnei ? s0 + kC : 0;
-    const bool more = cc + 1 < nch;
+    // (not when the window already shows that set to hold padding only)
+    const bool more = cc + 1 < nch &&
+                      (s0n - s0n % (kWindow / NB) != wbase || ((occ >> ((s0n - wbase) / kC)) & 1));
     double out[4] = {0.0, 0.0, 0.0, 0.0};   // this lane's dE/dR~ row
     if (tb.n > 0) {
       // the lanes whose records belong to pairs [base, base + np) read their products
