@@ -237,6 +237,7 @@ size_t dpc_nlist_workspace_bytes(int nloc, double box, double rc);
  *     (r2, j) ascending, for k < sel[beta]; the remaining slots hold -1.
  * The result does not depend on the order of the atoms inside the cell list
  * (the order is total), so it is reproducible bitwise.
+ *   nloc         at most 2^28 (else DPC_ENOTSUP)
  *   box, rc      require rc > 0 and box > 2 rc (else DPC_ERANGE)
  *   sel          host [ntypes], ntypes <= DPC_MAX_TYPES
  *   coord        device float64 [nloc][3] (any real values: positions are

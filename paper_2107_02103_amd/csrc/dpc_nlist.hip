@@ -39,22 +39,32 @@ struct alignas(16) NlAtom {      // an atom in cell order
   int j, type;
 };
 
-struct alignas(16) NlCand {      // a neighbour within r_c, as kept in LDS
-  uint64_t r2;                   // bits of r2 (>= 0: ordered like the value)
-  int j, type;
-};
+// A neighbour within r_c as kept in LDS: the bits of r2 (>= 0: ordered like
+// the value) in one array, type and index packed as type << 28 | j in another
+// (12 bytes per neighbour, so that three workgroups share a CU).
+constexpr int kJBits = 28;
+constexpr uint32_t kJMask = (1u << kJBits) - 1;
 
 struct NlGeo {
   int nloc, ntypes, nnei, nc, ncell;
   int lo_off, n_off;             // stencil offsets per axis: lo_off .. lo_off + n_off - 1
-  double box, rc2, inv_cs;
+  double box, rc2, inv_cs, inv_box;
   int sel[DPC_MAX_TYPES];
   int blk[DPC_MAX_TYPES + 1];    // first slot of each type block
 };
 
-__device__ __forceinline__ double min_image(double d, double box) {
+// d - box rint(d / box) with the quotient correctly rounded, as defined.
+// rint(d / box) is taken from d (1 / box) instead of a division whenever that
+// product lies more than 1e-6 away from a half-integer (and |q| < 2^20): the
+// two quotients differ by a few units in the last place (< 1e-9 there), so
+// both round to the same integer.  Otherwise (rare; NaN and infinities too)
+// the division decides.
+__device__ __forceinline__ double min_image(double d, const NlGeo& g) {
 #pragma clang fp contract(off)
-  return d - box * rint(d / box);
+  const double q = d * g.inv_box;
+  double n = rint(q);
+  if (!(fabs(q - n) < 0.499999 && fabs(q) < 1048576.0)) n = rint(d / g.box);
+  return d - g.box * n;
 }
 
 __device__ __forceinline__ int cell_axis(double x, const NlGeo& g) {
@@ -126,6 +136,26 @@ __global__ void nl_scatter_kernel(const NlGeo g, const double* __restrict__ coor
 
 __device__ __forceinline__ uint64_t ballot(bool b) { return __ballot(b); }
 
+// rank + 1 if (type, r2, j) of the packed neighbour (or2, ojt) is below
+// (t, r2, j) as unsigned words (the borrow
+// of the four-word subtraction), else rank.  r2 >= 0, so its bits order like
+// its value.  A subtraction chain keeps the whole comparison in the vector
+// unit; compares combined with mask logic would go through scalar registers.
+__device__ __forceinline__ unsigned count_before(uint64_t or2, uint32_t ojt, uint32_t j, uint32_t r2lo,
+                                                 uint32_t r2hi, uint32_t t, unsigned rank) {
+  uint32_t d;
+  asm("v_sub_co_u32 %0, vcc, %2, %3\n\t"
+      "v_subb_co_u32 %0, vcc, %4, %5, vcc\n\t"
+      "v_subb_co_u32 %0, vcc, %6, %7, vcc\n\t"
+      "v_subb_co_u32 %0, vcc, %8, %9, vcc\n\t"
+      "v_addc_co_u32 %1, vcc, 0, %1, vcc"
+      : "=&v"(d), "+v"(rank)
+      : "v"(ojt & kJMask), "v"(j), "v"((uint32_t)or2), "v"(r2lo), "v"((uint32_t)(or2 >> 32)),
+        "v"(r2hi), "v"(ojt >> kJBits), "v"(t)
+      : "vcc");
+  return rank;
+}
+
 __device__ __forceinline__ int lanes_below(uint64_t m) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
 }
@@ -136,51 +166,94 @@ __global__ __launch_bounds__(64 * kNlWaves) void nl_list_kernel(
     const int* __restrict__ start, const NlAtom* __restrict__ sorted, int* __restrict__ nlist,
     int* __restrict__ status) {
 #pragma clang fp contract(off)
-  __shared__ NlCand cand[kNlWaves][kNlCap];
+  __shared__ uint64_t cand_r2[kNlWaves][kNlCap + 4];
+  __shared__ uint32_t cand_jt[kNlWaves][kNlCap + 4];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i = __builtin_amdgcn_readfirstlane((int)(blockIdx.x * kNlWaves + wave));
   if (i >= g.nloc) return;
-  NlCand* my = cand[wave];
+  uint64_t* my_r2 = cand_r2[wave];
+  uint32_t* my_jt = cand_jt[wave];
   const double xi = coord[3 * (size_t)i], yi = coord[3 * (size_t)i + 1], zi = coord[3 * (size_t)i + 2];
   const int ci = __builtin_amdgcn_readfirstlane(cell_of[i]);
   const int cx = ci / (g.nc * g.nc), cy = (ci / g.nc) % g.nc, cz = ci % g.nc;
 
   // candidates within rc, in the order they are met (n may pass kNlCap:
-  // the extra ones are counted, not kept)
+  // the extra ones are counted, not kept).  The stencil's cells are read as
+  // spans of `sorted`: the cells of one (x, y) column that are consecutive
+  // in z are consecutive there too, so a column is one span, or two where
+  // it wraps around the box.  Lane k < 2 n_off^2 holds span k (column k / 2,
+  // part k % 2, possibly empty); the loop walks the spans 64 atoms at a time
+  // and loads the next batch before it works on the current one.
+  const int nsp = 2 * g.n_off * g.n_off;
+  int sp0 = 0, sp1 = 0;
+  if (lane < nsp) {
+    const int col = lane >> 1, part = lane & 1;
+    const int ax = (cx + g.lo_off + col / g.n_off + g.nc) % g.nc;
+    const int ay = (cy + g.lo_off + col % g.n_off + g.nc) % g.nc;
+    const int base = (ax * g.nc + ay) * g.nc;
+    int c0 = 0, c1 = 0;                 // cells [c0, c1) of this column
+    if (g.nc < 3) {
+      if (part == 0) c1 = g.nc;
+    } else if (cz > 0 && cz < g.nc - 1) {
+      if (part == 0) { c0 = cz - 1; c1 = cz + 2; }
+    } else if (cz == 0) {
+      if (part == 0) { c0 = g.nc - 1; c1 = g.nc; } else { c0 = 0; c1 = 2; }
+    } else {
+      if (part == 0) { c0 = g.nc - 2; c1 = g.nc; } else { c0 = 0; c1 = 1; }
+    }
+    sp0 = start[base + c0];
+    sp1 = start[base + c1];
+  }
+  // the first batch at or after (span s, atom b) that holds atoms
+  auto advance = [&](int& s, int& b, int& e) __attribute__((always_inline)) {
+    while (b >= e && ++s < nsp) {
+      b = __builtin_amdgcn_readlane(sp0, s);
+      e = __builtin_amdgcn_readlane(sp1, s);
+    }
+  };
   int n = 0;
-  for (int ox = 0; ox < g.n_off; ++ox)
-    for (int oy = 0; oy < g.n_off; ++oy)
-      for (int oz = 0; oz < g.n_off; ++oz) {
-        const int ax = (cx + g.lo_off + ox + g.nc) % g.nc;
-        const int ay = (cy + g.lo_off + oy + g.nc) % g.nc;
-        const int az = (cz + g.lo_off + oz + g.nc) % g.nc;
-        const int c = (ax * g.nc + ay) * g.nc + az;
-        const int p0 = start[c], p1 = start[c + 1];
-        for (int b = p0; b < p1; b += 64) {
-          const int p = b + lane;
-          bool ok = false;
-          NlCand k{0, 0, 0};
-          if (p < p1) {
-            const NlAtom a = sorted[p];
-            const double dx = min_image(a.x - xi, g.box);
-            const double dy = min_image(a.y - yi, g.box);
-            const double dz = min_image(a.z - zi, g.box);
-            const double r2 = dx * dx + dy * dy + dz * dz;
-            ok = r2 < g.rc2 && a.j != i && a.type >= 0 && a.type < g.ntypes;
-            k.r2 = __builtin_bit_cast(uint64_t, r2);
-            k.j = a.j;
-            k.type = a.type;
-          }
-          const uint64_t m = ballot(ok);
-          const int pos = n + lanes_below(m);
-          if (ok && pos < kNlCap) my[pos] = k;
-          n += __popcll(m);
-        }
-      }
+  int s = 0, b = __builtin_amdgcn_readlane(sp0, 0), e = __builtin_amdgcn_readlane(sp1, 0);
+  advance(s, b, e);
+  NlAtom cur = sorted[s < nsp ? min(b + lane, g.nloc - 1) : 0];
+  while (s < nsp) {
+    int s2 = s, b2 = b + 64, e2 = e;
+    advance(s2, b2, e2);
+    // every lane loads (an index inside the array), so that no load is conditional
+    const NlAtom nxt = sorted[s2 < nsp ? min(b2 + lane, g.nloc - 1) : 0];
+    bool ok = false;
+    uint64_t kr2 = 0;
+    uint32_t kjt = 0;
+    if (b + lane < e) {
+      const double dx = min_image(cur.x - xi, g);
+      const double dy = min_image(cur.y - yi, g);
+      const double dz = min_image(cur.z - zi, g);
+      const double r2 = dx * dx + dy * dy + dz * dz;
+      ok = r2 < g.rc2 && cur.j != i && cur.type >= 0 && cur.type < g.ntypes;
+      kr2 = __builtin_bit_cast(uint64_t, r2);
+      kjt = (uint32_t)cur.type << kJBits | (uint32_t)cur.j;
+    }
+    const uint64_t msk = ballot(ok);
+    const int pos = n + lanes_below(msk);
+    if (ok && pos < kNlCap) {
+      my_r2[pos] = kr2;
+      my_jt[pos] = kjt;
+    }
+    n += __popcll(msk);
+    cur = nxt;
+    s = s2;
+    b = b2;
+    e = e2;
+  }
+  const int m = n < kNlCap ? n : kNlCap;
+  // four entries that rank after every neighbour (type field 15) after the
+  // kept ones, so that the ranking below reads the list four at a time
+  if (lane < 4) {
+    my_r2[m + lane] = ~0ull;
+    my_jt[m + lane] = ~0u;
+  }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  const int m = n < kNlCap ? n : kNlCap;
 
   // neighbours of each type (all of them, before truncation)
   int cnt[DPC_MAX_TYPES];
@@ -188,34 +261,53 @@ __global__ __launch_bounds__(64 * kNlWaves) void nl_list_kernel(
   for (int t = 0; t < DPC_MAX_TYPES; ++t) cnt[t] = 0;
   for (int b = 0; b < m; b += 64) {
     const int q = b + lane;
-    const int ty = q < m ? my[q].type : -1;
+    const int ty = q < m ? (int)(my_jt[q] >> kJBits) : -1;
 #pragma unroll
     for (int t = 0; t < DPC_MAX_TYPES; ++t) cnt[t] += __popcll(ballot(ty == t));
   }
 
-  // slot of each kept neighbour: its rank among the neighbours of its type,
-  // by (r2, j); four candidates per lane per pass over all m
+  // slot of each kept neighbour: its rank among the neighbours of its type
+  // by (r2, j), i.e. its rank among all of them by (type, r2, j) less the
+  // number of neighbours of smaller types; up to four candidates per lane
+  // per pass over all m, four list entries per step
   int* row = nlist + (size_t)i * g.nnei;
   for (int b = 0; b < m; b += 256) {
-    NlCand own[4];
-    int rank[4];
+    uint64_t own_r2[4];
+    uint32_t own_jt[4];
+    unsigned rank[4];
+    const int nu = min(4, (m - b + 63) / 64);   // candidate sets of this pass
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int q = b + 64 * u + lane;
-      own[u] = q < m ? my[q] : NlCand{~0ull, -1, -1};
+      own_r2[u] = q < m ? my_r2[q] : ~0ull;
+      own_jt[u] = q < m ? my_jt[q] : ~0u;
       rank[u] = 0;
-    }
-    for (int e = 0; e < m; ++e) {
-      const NlCand o = my[e];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        rank[u] += (o.type == own[u].type &&
-                    (o.r2 < own[u].r2 || (o.r2 == own[u].r2 && o.j < own[u].j))) ? 1 : 0;
+      for (int t = 0; t < DPC_MAX_TYPES; ++t)
+        rank[u] -= (uint32_t)t < (own_jt[u] >> kJBits) ? (unsigned)cnt[t] : 0u;
+    }
+    for (int e = 0; e < m; e += 4) {
+      uint64_t o_r2[4];
+      uint32_t o_jt[4];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        o_r2[v] = my_r2[e + v];
+        o_jt[v] = my_jt[e + v];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (u >= nu) break;
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          rank[u] = count_before(o_r2[v], o_jt[v], own_jt[u] & kJMask, (uint32_t)own_r2[u],
+                                 (uint32_t)(own_r2[u] >> 32), own_jt[u] >> kJBits, rank[u]);
+      }
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const int t = own[u].type;
-      if (t >= 0 && rank[u] < g.sel[t]) row[g.blk[t] + rank[u]] = own[u].j;
+      const int q = b + 64 * u + lane;
+      const int t = (int)(own_jt[u] >> kJBits);
+      if (q < m && (int)rank[u] < g.sel[t]) row[g.blk[t] + (int)rank[u]] = (int)(own_jt[u] & kJMask);
     }
   }
   // empty slots of each block
@@ -269,7 +361,8 @@ constexpr NlLayout layout(int nloc, int ncell) {
 int make_geo(int nloc, int ntypes, const int* sel, double box, double rc, NlGeo* g) {
 #pragma clang fp contract(off)
   if (nloc < 0 || ntypes < 1 || !sel) return DPC_EINVAL;
-  if (ntypes > DPC_MAX_TYPES) return DPC_ENOTSUP;
+  // neighbour indices are kept in kJBits bits
+  if (ntypes > DPC_MAX_TYPES || nloc > (1 << kJBits)) return DPC_ENOTSUP;
   if (!(std::isfinite(box) && std::isfinite(rc) && rc > 0.0 && box > 2.0 * rc)) return DPC_ERANGE;
   int64_t nnei = 0;
   for (int t = 0; t < ntypes; ++t) {
@@ -291,6 +384,7 @@ int make_geo(int nloc, int ntypes, const int* sel, double box, double rc, NlGeo*
   g->box = box;
   g->rc2 = rc * rc;
   g->inv_cs = g->nc / box;
+  g->inv_box = 1.0 / box;
   return DPC_OK;
 }
 

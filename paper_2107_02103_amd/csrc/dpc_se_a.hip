@@ -1119,14 +1119,16 @@ __device__ __forceinline__ void descriptor_bwd_operands(const Geo& g, int i0,
     }
     const bool cv = col < m2;
     const int cc = cv ? col : 0;
-#pragma unroll 4
-    for (int p = 0; p < np; ++p) {
-      const int mp = 4 * p + kk;
-      const bool ok = mp < m1;
-      const int mc = ok ? mp : 0;
-      const double bt = ok ? Ta[mc * 4 + x] : 0.0;
-      const double at = ok && cv ? __builtin_nontemporal_load(Da + (size_t)mc * m2 + cc) : 0.0;
-      acc[0] = mfma4(at, bt, acc[0]);
+    for (int p0 = 0; p0 < np; p0 += 4) {   // four K steps at a time (zeros past M1)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int mp = 4 * (p0 + u) + kk;
+        const bool ok = mp < m1;
+        const int mc = ok ? mp : 0;
+        const double bt = ok ? Ta[mc * 4 + x] : 0.0;
+        const double at = ok && cv ? __builtin_nontemporal_load(Da + (size_t)mc * m2 + cc) : 0.0;
+        acc[0] = mfma4(at, bt, acc[0]);
+      }
     }
 #pragma unroll
     for (int s = 0; s < S; ++s) A[a][s] = live && 16 * s + (lane >> 2) < m1 ? acc[s] : 0.0;

@@ -332,7 +332,8 @@ def test_nlist_entry_point_validates_before_launch():
     cases = [(dict(box=10.0), B.DPC_ERANGE), (dict(rc=0.0), B.DPC_ERANGE), (dict(rc=float("nan")), B.DPC_ERANGE),
              (dict(nloc=-1), B.DPC_EINVAL), (dict(sel=[8, -1]), B.DPC_EINVAL), (dict(coord=0), B.DPC_EINVAL),
              (dict(workspace_bytes=nb - 1), B.DPC_EINVAL), (dict(workspace=fake * 256 + 16), B.DPC_EINVAL),
-             (dict(ntypes=9, sel=[1] * 9), B.DPC_ENOTSUP), (dict(nlist=0), B.DPC_EINVAL)]
+             (dict(ntypes=9, sel=[1] * 9), B.DPC_ENOTSUP), (dict(nlist=0), B.DPC_EINVAL),
+             (dict(nloc=(1 << 28) + 1), B.DPC_ENOTSUP)]     # neighbour indices take 28 bits
     for kw, code in cases:
         a = dict(base); a.update(kw)
         with pytest.raises(P.DpcError) as e:
