@@ -212,11 +212,13 @@ int dpc_env_mat_a(void* stream, dpc_dtype dtype, int nloc, int ntypes, int nnei,
 
 /* Reverse slots of a neighbour list, for dpc_force_a: rev[i][s] = the slot of
  * i in the list of j = nlist[i][s], searched in the sel block of i's type
- * (sel as in dpc_se_a_tab_fwd), or -1 if i is not there (and for padding).
- * Lists sorted by distance within each block are searched by bisection;
- * other orders are scanned, with the same result.  Build it once per
- * neighbour list.
- *   coord device float64 [nloc][3], cubic box of edge `box` (minimum image)
+ * (sel as in dpc_se_a_tab_fwd), or -1 if i is not there (and for padding);
+ * if j's block holds i more than once, one of those slots.  In lists sorted
+ * by distance within each block i sits near j's rank in i's list, where the
+ * search looks first; other orders are scanned, with the same result.
+ * Build it once per neighbour list.
+ *   coord, box  as for the other calls (validated; the search reads only the
+ *               lists and atype)
  *   rev   device out int32 [nloc][nnei]                                      */
 int dpc_nlist_reverse(void* stream, int nloc, int ntypes, const int* sel, double box,
                       const double* coord, const int* atype, const int* nlist, int* rev);

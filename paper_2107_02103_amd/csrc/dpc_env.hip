@@ -127,50 +127,93 @@ __global__ __launch_bounds__(256) void env_mat_kernel(const EnvGeo g, int chunks
   }
 }
 
-// rev[i][s] = slot of i in the list of j = nlist[i][s] (in the sel block of
-// i's type), -1 if absent.  The block is searched by distance from j (lists
-// sorted by distance within a block find it after a binary search and a
-// short scan); if that fails the whole block is scanned, so the result does
-// not depend on the order.
-__global__ __launch_bounds__(256) void reverse_kernel(const EnvGeo g, const double* __restrict__ coord,
-                                                      const int* __restrict__ atype,
+// rev[i][s] = slot of i in the list of j = nlist[i][s], in the sel block of
+// i's type, or -1.  rev starts as -1 everywhere (fill_kernel).  A pair found
+// in both lists gives both entries, rev[i][s] = k and rev[j][k] = s, so each
+// pair is searched once, by the wavefront of its smaller atom i < j (the
+// other one skips it; a pair that only one list holds is searched by that
+// list's atom when it is the smaller one, and else stays -1, which is then
+// right).  The wavefront takes its pairs eight at a time, and for each the
+// whole wavefront reads the two 128-byte lines of j's block around where i
+// is expected (i's rank in j's list is close to j's rank in i's list: the
+// same distance orders both) and looks for i with one ballot; the eight
+// window reads are issued together.  A miss (lists in another order, ranks
+// further apart) scans j's whole block.
+constexpr int kRevGroup = 8;
+__global__ void fill_kernel(int64_t n, int v, int* __restrict__ p) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e < n) p[e] = v;
+}
+
+__global__ __launch_bounds__(256) void reverse_kernel(const EnvGeo g, const int* __restrict__ atype,
                                                       const int* __restrict__ nlist,
                                                       int* __restrict__ rev) {
-  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= (int64_t)g.nloc * g.nnei) return;
-  const int i = (int)(e / g.nnei);
-  const int j = nlist[e];
-  int found = -1;
-  const int t = atype[i];
-  if (j >= 0 && j < g.nloc && t >= 0 && t < g.ntypes) {
-    const double* cj = coord + 3 * (size_t)j;
-    const int* lj = nlist + (size_t)j * g.nnei;
-    double d[3];
-    min_image(g, cj, coord + 3 * (size_t)i, d);
-    const double r2 = d[0] * d[0] + d[1] * d[1] + d[2] * d[2];
-    auto dist2 = [&](int k) -> double {   // distance^2 from j of the atom in slot k (inf for padding)
-      const int a = lj[k];
-      if (a < 0 || a >= g.nloc) return INFINITY;
-      double q[3];
-      min_image(g, cj, coord + 3 * (size_t)a, q);
-      return q[0] * q[0] + q[1] * q[1] + q[2] * q[2];
-    };
-    const int b0 = g.blk[t], b1 = g.blk[t + 1];
-    const double tol = 1e-12 * r2;
-    int lo = b0, hi = b1;                 // first slot with dist2 >= r2 - tol
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (dist2(mid) < r2 - tol) lo = mid + 1;
-      else hi = mid;
+  const int lane = threadIdx.x & 63;
+  const int i = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6));
+  if (i >= g.nloc) return;
+  const int t = __builtin_amdgcn_readfirstlane(atype[i]);
+  if (t < 0 || t >= g.ntypes) return;       // its slots stay -1
+  const int b0 = g.blk[t], b1 = g.blk[t + 1];
+  const int wlo = b0, whi = b1 - 32 > b0 ? b1 - 32 : b0;     // window centres start here
+  const int* li = nlist + (size_t)i * g.nnei;
+  int* ri = rev + (size_t)i * g.nnei;
+  int jn = lane < g.nnei ? li[lane] : -1;      // the next batch's slots, loaded ahead
+  for (int s0 = 0; s0 < g.nnei; s0 += 64) {
+    const int s = s0 + lane;
+    const int j = jn;
+    jn = s + 64 < g.nnei ? li[s + 64] : -1;
+    const bool mine = j > i && j < g.nloc;
+    int found = -1, tmine = -1;       // this lane's pair: slot of i in j's list, j's type
+    uint64_t todo = __ballot(mine);
+    while (todo) {
+      int src[kRevGroup], jj[kRevGroup], tj[kRevGroup], w0[kRevGroup], v[kRevGroup];
+#pragma unroll
+      for (int q = 0; q < kRevGroup; ++q) {
+        src[q] = todo ? (int)__builtin_ctzll(todo) : -1;
+        todo &= todo ? todo - 1 : 0;
+        jj[q] = src[q] >= 0 ? __builtin_amdgcn_readlane(j, src[q]) : 0;
+        tj[q] = atype[jj[q]];          // uniform: a scalar load beside the window's
+        // j's place in i's list, relative to the start of its block there
+        const int sj = s0 + (src[q] >= 0 ? src[q] : 0);
+        int bs = 0;
+#pragma unroll
+        for (int u = 1; u < DPC_MAX_TYPES; ++u) bs = (u < g.ntypes && sj >= g.blk[u]) ? g.blk[u] : bs;
+        // 32 slots centred where i is expected, clamped into the block, read
+        // as the two 32-entry groups of the row that hold them
+        const int c = b0 + (sj - bs) - 16;
+        const int ca = c < wlo ? wlo : (c > whi ? whi : c);
+        w0[q] = ca & ~31;
+        // every lane reads an entry inside j's row; those outside the block are masked
+        const int k = w0[q] + lane;
+        v[q] = nlist[(size_t)jj[q] * g.nnei + (k < g.nnei ? k : g.nnei - 1)];
+        v[q] = k >= b0 && k < b1 ? v[q] : -1;
+      }
+#pragma unroll
+      for (int q = 0; q < kRevGroup; ++q) {
+        if (src[q] < 0) break;
+        const uint64_t hit = __ballot(v[q] == i);
+        int kk = hit ? w0[q] + (int)__builtin_ctzll(hit) : -1;
+        for (int c0 = b0; kk < 0 && c0 < b1; c0 += 64) {   // not in the window: the whole block
+          const int k = c0 + lane;
+          const int e = k < b1 ? nlist[(size_t)jj[q] * g.nnei + k] : -1;
+          const uint64_t h = __ballot(e == i);
+          kk = h ? c0 + (int)__builtin_ctzll(h) : -1;
+        }
+        if (lane == src[q]) {
+          found = kk;
+          tmine = tj[q];
+        }
+      }
     }
-    for (int k = lo; k < b1 && found < 0; ++k) {
-      if (lj[k] == i) found = k;
-      else if (dist2(k) > r2 + tol) break;
+    // one store instruction each per batch: the found slots, and their
+    // reverses, j's slot in i's list, where it lies in the block of j's
+    // type (where that search would look)
+    if (found >= 0) {
+      ri[s] = found;
+      if (tmine >= 0 && tmine < g.ntypes && s >= g.blk[tmine] && s < g.blk[tmine + 1])
+        rev[(size_t)j * g.nnei + found] = s;
     }
-    for (int k = b0; k < b1 && found < 0; ++k)
-      if (lj[k] == i) found = k;
   }
-  rev[e] = found;
 }
 
 // one wavefront per atom; lane l takes slots l, l + 64, ...
@@ -296,13 +339,6 @@ int make_env_geo(int nloc, int ntypes, int nnei, double box, double rc, double r
   return DPC_OK;
 }
 
-int slot_grid(const EnvGeo& g, dim3* grid) {
-  const int64_t n = ((int64_t)g.nloc * g.nnei + 255) / 256;
-  if (n >= (int64_t(1) << 31)) return DPC_ENOTSUP;
-  *grid = dim3((unsigned)n);
-  return DPC_OK;
-}
-
 }  // namespace
 
 extern "C" int dpc_env_mat_a(void* stream, dpc_dtype dtype, int nloc, int ntypes, int nnei,
@@ -360,11 +396,12 @@ extern "C" int dpc_nlist_reverse(void* stream, int nloc, int ntypes, const int* 
   for (int t = ntypes; t <= DPC_MAX_TYPES; ++t) g.blk[t] = off;
   if (nloc == 0) return DPC_OK;
   if (!coord || !atype || !nlist || !rev) return DPC_EINVAL;
-  dim3 grid;
-  if (slot_grid(g, &grid) != DPC_OK) return DPC_ENOTSUP;
+  const int64_t nslot = (int64_t)nloc * nnei;
+  if ((nslot + 255) / 256 >= (int64_t(1) << 31)) return DPC_ENOTSUP;
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
-  hipLaunchKernelGGL(reverse_kernel, grid, dim3(256), 0, s, g, coord, atype, nlist, rev);
+  hipLaunchKernelGGL(fill_kernel, dim3((unsigned)((nslot + 255) / 256)), dim3(256), 0, s, nslot, -1, rev);
+  hipLaunchKernelGGL(reverse_kernel, dim3((nloc + 3) / 4), dim3(256), 0, s, g, atype, nlist, rev);
   return dpc_internal_launch_status();
 }
 

@@ -142,3 +142,26 @@ def test_deterministic_and_empty():
     nl = torch.zeros((0, 10), dtype=torch.int32, device="cuda")
     ws = torch.zeros(256, dtype=torch.uint8, device="cuda")
     assert P.dpc_nlist_build(0, 0, 1, [10], 20.0, 5.0, e, t, ws, 256, nl) == (0, 0)
+
+
+def test_half_box_differences():
+    # coordinate differences of exactly half a box and one unit in the last
+    # place either side: the minimum image's rint(d / box) sits on or next to
+    # a tie there, where the kernel takes the quotient from a division
+    rng = np.random.default_rng(11)
+    box, rc = 20.0, 9.5
+    base = rng.uniform(0, box, size=(60, 3))
+    half = np.array([0.5 * box, 0.0, 0.0])
+    coord = [base]
+    for step in (-1, 0, 1):
+        shifted = base + half
+        shifted[:, 0] = np.nextafter(shifted[:, 0], np.inf * step) if step else shifted[:, 0]
+        coord.append(shifted)
+    coord.append(base + np.array([0.5 * box, 0.5 * box, -0.5 * box]))
+    coord = np.concatenate(coord)
+    atype = rng.integers(0, 2, size=len(coord)).astype(np.int32)
+    sel = (300, 300)
+    got, st = _gpu(coord, atype, sel, box, rc, wait=False)
+    ref, cnt, over = onl.neighbour_list(coord, atype, sel, box, rc)
+    assert st == (over, 0)
+    np.testing.assert_array_equal(got, ref)
