@@ -150,6 +150,77 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// The NB atoms of a wavefront.  A workgroup takes kWaves * NB consecutive
+// atoms.  With several types it hands them to its wavefronts grouped by type
+// (atoms of an invalid type after the others, index order inside a group),
+// so that the atoms of one wavefront share their tables as often as
+// possible: more records per interval.  An atom's records and sums do not
+// depend on which atoms share its wavefront; only the chunk set its sums
+// start from does (the start rotates with the wavefront), i.e. the order of
+// rounding.  idx[a] is the atom's index, -1 past
+// nloc (those come last); lane a < NB of `lanes` holds idx[a] as well, for
+// lookups with an index known only at run time (a register array indexed so
+// would go to scratch memory).
+template <int NB>
+struct WaveAtoms {
+  int idx[NB];
+  int lanes;
+};
+
+template <int NB, bool kOne>
+__device__ __forceinline__ WaveAtoms<NB> wave_atoms(const Geo& g, const int* __restrict__ atype,
+                                                    int lane, int wave) {
+  constexpr int kG = kWaves * NB;
+  static_assert(kG <= kLanes, "one lane per atom of the workgroup");
+  WaveAtoms<NB> w;
+  const int base = (int)blockIdx.x * kG;
+  if (kOne || g.ntypes == 1) {
+#pragma unroll
+    for (int a = 0; a < NB; ++a) {
+      const int i = base + wave * NB + a;
+      w.idx[a] = __builtin_amdgcn_readfirstlane(i < g.nloc ? i : -1);
+    }
+    const int il = base + wave * NB + lane;
+    w.lanes = lane < NB && il < g.nloc ? il : -1;
+    return w;
+  }
+  const int at = base + lane;
+  const bool in = lane < kG && at < g.nloc;
+  int key = 0;
+  if (in) {
+    const int t = atype[at];
+    key = t >= 0 && t < g.ntypes ? t : g.ntypes;
+  }
+  // position of this lane's atom in the order (key, index)
+  const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  int pos = 0;
+#pragma unroll
+  for (int v = 0; v <= DPC_MAX_TYPES; ++v) {
+    const uint64_t m = __ballot(in && key == v);
+    pos += v < key ? __popcll(m) : (v == key ? __popcll(m & below) : 0);
+  }
+  w.lanes = -1;
+#pragma unroll
+  for (int a = 0; a < NB; ++a) {
+    const uint64_t hit = __ballot(in && pos == wave * NB + a);
+    w.idx[a] = __builtin_amdgcn_readfirstlane(hit ? base + (int)__builtin_ctzll(hit) : -1);
+    w.lanes = lane == a ? w.idx[a] : w.lanes;
+  }
+  return w;
+}
+
+// idx[a] for an index a in [0, NB) that is the same in every lane
+template <int NB>
+__device__ __forceinline__ int atom_of(const WaveAtoms<NB>& w, int a) {
+  return __builtin_amdgcn_readlane(w.lanes, a);
+}
+
+// idx[a] for a per-lane index a in [0, NB)
+template <int NB>
+__device__ __forceinline__ int lane_atom_of(const WaveAtoms<NB>& w, int a) {
+  return __builtin_amdgcn_ds_bpermute(a << 2, w.lanes);
+}
+
 __device__ __forceinline__ int lanes_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
                                    __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
@@ -223,7 +294,7 @@ __device__ __forceinline__ int split_at(const int (&p)[2], int b) {
 constexpr int kWindow = 32 * kLanes;
 
 template <int NB>
-__device__ __forceinline__ uint32_t valid_window(const Geo& g, int i0, int wbase,
+__device__ __forceinline__ uint32_t valid_window(const Geo& g, const WaveAtoms<NB>& wa, int wbase,
                                                  const int* __restrict__ nlist, int lane) {
   constexpr int W = kWindow / NB;
   constexpr int kGroup = 8;   // loads in flight at once
@@ -231,21 +302,19 @@ __device__ __forceinline__ uint32_t valid_window(const Geo& g, int i0, int wbase
 #pragma unroll 1
   for (int k0 = 0; k0 < 32; k0 += kGroup) {
     int v[kGroup];
+    bool in[kGroup];
 #pragma unroll
     for (int q = 0; q < kGroup; ++q) {
       const int il = lane + kLanes * (k0 + q);
-      const int a = il / W, j = wbase + il % W;
-      const bool in = i0 + a < g.nloc && j < g.nnei;
-      // out-of-range entries read slot 0 of atom i0 (always present) and are masked below
-      v[q] = __builtin_nontemporal_load(nlist + (in ? (size_t)(i0 + a) * g.nnei + j
-                                                    : (size_t)i0 * g.nnei));
+      // W is a multiple of 64: the atom slot is the same in every lane
+      const int ia = atom_of<NB>(wa, kLanes * (k0 + q) / W), j = wbase + il % W;
+      in[q] = ia >= 0 && j < g.nnei;
+      // out-of-range entries read slot 0 of atom idx[0] (always present) and are masked below
+      v[q] = __builtin_nontemporal_load(nlist + (in[q] ? (size_t)ia * g.nnei + j
+                                                       : (size_t)wa.idx[0] * g.nnei));
     }
 #pragma unroll
-    for (int q = 0; q < kGroup; ++q) {
-      const int il = lane + kLanes * (k0 + q);
-      const bool in = i0 + il / W < g.nloc && wbase + il % W < g.nnei;
-      vm |= (in && v[q] >= 0 ? 1u : 0u) << (k0 + q);
-    }
+    for (int q = 0; q < kGroup; ++q) vm |= (in[q] && v[q] >= 0 ? 1u : 0u) << (k0 + q);
   }
   return vm;
 }
@@ -300,9 +369,10 @@ __device__ __forceinline__ void store_row(TA* p, const TA (&v)[4]) {
 }
 
 // Zero dE/dR~ rows of a chunk set without valid slots (slots s0 + lane % kC
-// of atom lane / kC; atoms past nloc or of an invalid type are skipped).
+// of atom `atom`, the wavefront's atom lane / kC; atoms past nloc or of an
+// invalid type are skipped).
 template <typename TA, int NB>
-__device__ __forceinline__ void zero_rows(const Geo& g, const int (&ai)[NB], int i0, int s0,
+__device__ __forceinline__ void zero_rows(const Geo& g, const int (&ai)[NB], int atom, int s0,
                                           TA* __restrict__ dR, int lane) {
   constexpr int kC = kLanes / NB;
   const int a = lane / kC, j = s0 + lane % kC;
@@ -312,19 +382,20 @@ __device__ __forceinline__ void zero_rows(const Geo& g, const int (&ai)[NB], int
     if (b == a) at = ai[b];
   if (at >= 0 && j < g.nnei) {
     const TA z[4] = {(TA)0, (TA)0, (TA)0, (TA)0};
-    store_row(dR + ((size_t)(i0 + a) * g.nnei + j) * 4, z);
+    store_row(dR + ((size_t)atom * g.nnei + j) * 4, z);
   }
 }
 
 // Merge slots [s0, s0 + 64/NB) of the wave's NB atoms into W and build the
-// run tables.  Lane l covers slot s0 + l % (64/NB) of atom l / (64/NB).  In
+// run tables.  Lane l covers slot s0 + l % (64/NB) of the wavefront's atom
+// l / (64/NB), whose index is `atom`.  In
 // the backward pass (kBwd) clamped records get a zero R~ row.  With kPairs
 // the lane also gets the index of its record's (interval, atom) pair among
 // the chunk set's pairs in merged order (`pair`, -1 without a record), a
 // pair being a maximal group of records with equal key and atom, and keeps
 // its record in registers (`mine`) instead of writing it to z.
 template <typename TI, typename TA, int NB, bool kBwd, bool kOne, bool kPairs = false>
-__device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[NB], int i0,
+__device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[NB], int atom,
                                                   int s0, int wbase, uint32_t vm,
                                                   const TI* __restrict__ em, Rec<TI>* z,
                                                   ChunkScratch& W, int lane,
@@ -344,7 +415,7 @@ __device__ __forceinline__ Tables build_chunk_set(const Geo& g, const int (&ai)[
   if constexpr (kPairs) rec = Rec<TI>{0.0, 0.0, {(TI)0, (TI)0, (TI)0, (TI)0}};
   int key = 0;
   if (at >= 0 && j < g.nnei) {
-    const size_t row = (size_t)(i0 + a) * g.nnei + j;
+    const size_t row = (size_t)atom * g.nnei + j;
     valid = (holder >> (il >> 6)) & 1;
     if (valid) {
       if (use_pre) {    // the caller has loaded the row already
@@ -495,8 +566,9 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_fwd_kernel(
   constexpr int kC = kLanes / NB;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int i0 = __builtin_amdgcn_readfirstlane((blockIdx.x * kWaves + wave) * NB);
-  if (i0 >= g.nloc) return;
+  const WaveAtoms<NB> wa = wave_atoms<NB, kOne>(g, atype, lane, wave);
+  if (wa.idx[0] < 0) return;
+  const int my_atom = lane_atom_of<NB>(wa, lane / kC);   // the atom of this lane's chunk-set slots
   const int nnei = g.nnei, m1 = g.m1, m2 = g.m2, ld = g.ld;
   const uint32_t zoff = __builtin_amdgcn_readfirstlane(wave * (uint32_t)fwd_wave_bytes<TI, TA>(m1));
   unsigned char* wb = smem + zoff;
@@ -507,9 +579,9 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_fwd_kernel(
   int ai[NB];
 #pragma unroll
   for (int a = 0; a < NB; ++a) {
-    const int i = i0 + a;
+    const int i = wa.idx[a];
     ai[a] = -1;
-    if (i < g.nloc) {
+    if (i >= 0) {
       const int t = __builtin_amdgcn_readfirstlane(atype[i]);
       if (t < 0 || t >= g.ntypes) {  // invalid type: the atom's outputs become NaN
         const TA nan = (TA)NAN;
@@ -545,11 +617,11 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_fwd_kernel(
   for (int cc = 0, wbase = -1; cc < nch; ++cc, s0 = s0 + kC < nnei ? s0 + kC : 0) {
     if (s0 - s0 % (kWindow / NB) != wbase) {  // window of nlist signs holding s0
       wbase = s0 - s0 % (kWindow / NB);
-      vm = valid_window<NB>(g, i0, wbase, nlist, lane);
+      vm = valid_window<NB>(g, wa, wbase, nlist, lane);
       occ = occupied_chunks<NB>(vm);
     }
     if (!((occ >> ((s0 - wbase) / kC)) & 1)) continue;   // padding only
-    const Tables tb = build_chunk_set<TI, TA, NB, false, kOne>(g, ai, i0, s0, wbase, vm, em, W.z, W.s, lane);
+    const Tables tb = build_chunk_set<TI, TA, NB, false, kOne>(g, ai, my_atom, s0, wbase, vm, em, W.z, W.s, lane);
     if (tb.n == 0) continue;
     load_coef<TI, CPL>(rs, key_offset(readlane(tb.vk, 0)), ld, voff, cfA);
     int r = 0;
@@ -609,7 +681,7 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_fwd_kernel(
   const int m_step = 64 / m2, n_step = 64 % m2;
 #pragma unroll
   for (int a = 0; a < NB; ++a) {
-    const int i = i0 + a;
+    const int i = wa.idx[a];
     if (ai[a] < 0) continue;
     wave_sync();
 #pragma unroll
@@ -706,8 +778,9 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
   constexpr int PS = part_stride<TA>();
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int i0 = __builtin_amdgcn_readfirstlane((blockIdx.x * kWaves + wave) * NB);
-  if (i0 >= g.nloc) return;
+  const WaveAtoms<NB> wa = wave_atoms<NB, kOne>(g, atype, lane, wave);
+  if (wa.idx[0] < 0) return;
+  const int my_atom = lane_atom_of<NB>(wa, lane / kC);   // the atom of this lane's chunk-set slots
   const int nnei = g.nnei, m1 = g.m1, ld = g.ld;
   static_assert(16 * part_stride<TA>() * sizeof(TA) <= 2 * kBatch * kRedBlock, "step 2 rows");
   const uint32_t zoff = __builtin_amdgcn_readfirstlane(wave * (uint32_t)bwd_wave_bytes<TI>());
@@ -725,18 +798,18 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
   int ai[NB];
 #pragma unroll
   for (int a = 0; a < NB; ++a) {
-    const int i = i0 + a;
+    const int i = wa.idx[a];
     ai[a] = -1;
 #pragma unroll
     for (int h = 0; h < CPL; ++h) {
       const int m = lane * CPL + h;
 #pragma unroll
       for (int k = 0; k < 4; ++k)
-        dt[a][h][k] = (i < g.nloc && m < m1)
+        dt[a][h][k] = (i >= 0 && m < m1)
                           ? (TA)__builtin_nontemporal_load(dT + ((size_t)i * m1 + m) * 4 + k)
                           : (TA)0;
     }
-    if (i < g.nloc) {
+    if (i >= 0) {
       const int t = __builtin_amdgcn_readfirstlane(atype[i]);
       if (t < 0 || t >= g.ntypes) {  // invalid type: the atom's outputs become NaN
         for (int e = lane; e < nnei * 4; e += 64) dR[(size_t)i * nnei * 4 + e] = (TA)NAN;
@@ -781,14 +854,14 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
   for (int cc = 0, wbase = -1; cc < nch; ++cc, s0 = s0 + kC < nnei ? s0 + kC : 0) {
     if (s0 - s0 % (kWindow / NB) != wbase) {  // window of nlist signs holding s0
       wbase = s0 - s0 % (kWindow / NB);
-      vm = valid_window<NB>(g, i0, wbase, nlist, lane);
+      vm = valid_window<NB>(g, wa, wbase, nlist, lane);
       occ = occupied_chunks<NB>(vm);
     }
     if (!((occ >> ((s0 - wbase) / kC)) & 1)) {   // padding only: zero rows
-      zero_rows<TA, NB>(g, ai, i0, s0, dR, lane);
+      zero_rows<TA, NB>(g, ai, my_atom, s0, dR, lane);
       continue;
     }
-    const Tables tb = build_chunk_set<TI, TA, NB, true, kOne>(g, ai, i0, s0, wbase, vm, em, W.z, W.s, lane);
+    const Tables tb = build_chunk_set<TI, TA, NB, true, kOne>(g, ai, my_atom, s0, wbase, vm, em, W.z, W.s, lane);
     // Each lane writes the dE/dR~ row of its own slot (zero for padding) after
     // the chunk set's runs: consecutive lanes, consecutive rows, and no store
     // ahead of the coefficient loads whose waits would then include it.
@@ -800,7 +873,7 @@ __attribute__((amdgpu_waves_per_eu(CPL <= 2 ? 3 : 1))) void se_a_bwd_kernel(
 #pragma unroll
           for (int k = 0; k < 4; ++k) v[k] = src[k];
         }
-        store_row(dR + ((size_t)(i0 + lane / kC) * nnei + s0 + lane % kC) * 4, v);
+        store_row(dR + ((size_t)my_atom * nnei + s0 + lane % kC) * 4, v);
       }
     };
     if (tb.n == 0) {
@@ -1082,7 +1155,7 @@ __device__ __forceinline__ void wait_copies() {
 // get zeros.  T and dE/dD are read straight from memory (the second sum
 // re-reads dE/dD rows the first sum has just brought into the caches).
 template <int NB, int S>
-__device__ __forceinline__ void descriptor_bwd_operands(const Geo& g, int i0,
+__device__ __forceinline__ void descriptor_bwd_operands(const Geo& g, const WaveAtoms<NB>& wa,
                                                         const double* __restrict__ Tin,
                                                         const double* __restrict__ dD, int lane,
                                                         double (&A)[NB][S]) {
@@ -1094,8 +1167,8 @@ __device__ __forceinline__ void descriptor_bwd_operands(const Geo& g, int i0,
   const int col = 4 * x + b;              // second sum: the output channel of the lane's A row
 #pragma unroll
   for (int a = 0; a < NB; ++a) {
-    const bool live = i0 + a < g.nloc;
-    const int i = min(i0 + a, g.nloc - 1);
+    const bool live = wa.idx[a] >= 0;
+    const int i = live ? wa.idx[a] : wa.idx[0];
     const double* Ta = Tin + (size_t)i * m1 * 4;
     const double* Da = dD + (size_t)i * m1 * m2;
     double acc[S];
@@ -1156,8 +1229,9 @@ void se_a_bwd_mfma_kernel(const Geo g, const TI* __restrict__ coeff,
   constexpr int kC = kLanes / NB;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int i0 = __builtin_amdgcn_readfirstlane((blockIdx.x * kWaves + wave) * NB);
-  if (i0 >= g.nloc) return;
+  const WaveAtoms<NB> wa = wave_atoms<NB, kOne>(g, atype, lane, wave);
+  if (wa.idx[0] < 0) return;
+  const int my_atom = lane_atom_of<NB>(wa, lane / kC);   // the atom of this lane's chunk-set slots
   const int nnei = g.nnei, m1 = g.m1, ld = g.ld;
   constexpr int kPairSlots = pair_slots(NS);
   const uint32_t zoff = __builtin_amdgcn_readfirstlane(wave * (uint32_t)bwdm_wave_bytes(NS));
@@ -1179,21 +1253,21 @@ void se_a_bwd_mfma_kernel(const Geo g, const TI* __restrict__ coeff,
   // A operands: dT of the wave's atoms, transposed, zero past M1
   double A[NB][S];
   int ai[NB];
-  if constexpr (kFromD) descriptor_bwd_operands<NB, S>(g, i0, Tin, dD, lane, A);
+  if constexpr (kFromD) descriptor_bwd_operands<NB, S>(g, wa, Tin, dD, lane, A);
 #pragma unroll
   for (int a = 0; a < NB; ++a) {
-    const int i = i0 + a;
+    const int i = wa.idx[a];
     if constexpr (!kFromD) {
 #pragma unroll
       for (int s = 0; s < S; ++s) {
         const int m = channel(s);
-        A[a][s] = (i < g.nloc && m < m1)
+        A[a][s] = (i >= 0 && m < m1)
                       ? (double)__builtin_nontemporal_load(dT + ((size_t)i * m1 + m) * 4 + x)
                       : 0.0;
       }
     }
     ai[a] = -1;
-    if (i < g.nloc) {
+    if (i >= 0) {
       const int t = __builtin_amdgcn_readfirstlane(atype[i]);
       if (t < 0 || t >= g.ntypes) {  // invalid type: the atom's outputs become NaN
         for (int e = lane; e < nnei * 4; e += 64) dR[(size_t)i * nnei * 4 + e] = (TO)NAN;
@@ -1223,17 +1297,17 @@ void se_a_bwd_mfma_kernel(const Geo g, const TI* __restrict__ coeff,
   for (int cc = 0, wbase = -1; cc < nch; ++cc, s0 = s0 + kC < nnei ? s0 + kC : 0) {
     if (s0 - s0 % (kWindow / NB) != wbase) {  // window of nlist signs holding s0
       wbase = s0 - s0 % (kWindow / NB);
-      vm = valid_window<NB>(g, i0, wbase, nlist, lane);
+      vm = valid_window<NB>(g, wa, wbase, nlist, lane);
       occ = occupied_chunks<NB>(vm);
     }
     if (!((occ >> ((s0 - wbase) / kC)) & 1)) {   // padding only: zero rows
-      zero_rows<TO, NB>(g, ai, i0, s0, dR, lane);
+      zero_rows<TO, NB>(g, ai, my_atom, s0, dR, lane);
       continue;
     }
     int pair;
     Rec<TI> mine;
     const Tables tb = build_chunk_set<TI, double, NB, true, kOne, true>(
-        g, ai, i0, s0, wbase, vm, em, nullptr, W, lane, &pair, &mine, pre_s0 == s0, pre);
+        g, ai, my_atom, s0, wbase, vm, em, nullptr, W, lane, &pair, &mine, pre_s0 == s0, pre);
     // the rows of the next chunk set are loaded during this one's last run
     const int s0n = s0 + kC < nnei ? s0 + kC : 0;
     // (not when the window already shows that set to hold padding only)
@@ -1311,7 +1385,7 @@ void se_a_bwd_mfma_kernel(const Geo g, const TI* __restrict__ coeff,
         if constexpr (!kLast) {
           fetch(next_off(r + 1));
         } else if (more) {
-          const int ia = min(i0 + lane / kC, g.nloc - 1), j = min(s0n + lane % kC, nnei - 1);
+          const int ia = my_atom >= 0 ? my_atom : wa.idx[0], j = min(s0n + lane % kC, nnei - 1);
           load_row(em + ((size_t)ia * nnei + j) * 4, pre);
           pre_s0 = s0n;
         }
@@ -1354,7 +1428,7 @@ void se_a_bwd_mfma_kernel(const Geo g, const TI* __restrict__ coeff,
     // each lane writes the dE/dR~ row of its own slot (zero for padding)
     if (tb.rank >= -1) {
       const TO o[4] = {(TO)out[0], (TO)out[1], (TO)out[2], (TO)out[3]};
-      store_row(dR + ((size_t)(i0 + lane / kC) * nnei + s0 + lane % kC) * 4, o);
+      store_row(dR + ((size_t)my_atom * nnei + s0 + lane % kC) * 4, o);
     }
     wave_sync();
   }

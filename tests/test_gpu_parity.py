@@ -257,3 +257,25 @@ def test_coefficients_past_the_buffer_are_not_read(m1):
     got = tuple(t.cpu().numpy() for t in (T, D, dR))
     assert all(np.isfinite(g).all() for g in got)
     _check(x, np.arange(64), got, "f64")
+
+
+@pytest.mark.parametrize("dtype", ["f64", "f32acc64", "f32"])
+def test_mixed_and_invalid_types_in_one_workgroup(dtype):
+    # three types in random order, plus atoms of invalid type (-1 and
+    # ntypes): a workgroup hands its atoms to its wavefronts grouped by type,
+    # invalid ones last; every valid atom still matches the oracle, every
+    # invalid one gets NaN outputs, and runs repeat bitwise
+    x = _synthetic(77, (30, 20, 14), 100, 16, seed=21)
+    rng = np.random.default_rng(5)
+    x.atype[:] = rng.integers(0, 3, size=77).astype(np.int32)
+    bad = np.array([3, 16, 17, 40, 76])
+    x.atype[bad[:3]] = -1
+    x.atype[bad[3:]] = 3
+    T, D, dR = (t.cpu().numpy() for t in _run_gpu(x, dtype)[2])
+    for a in (T, D, dR):
+        assert np.isnan(a[bad]).all()
+    good = np.setdiff1d(np.arange(77), bad)
+    _check(x, good, (T, D, dR), dtype)
+    T2, D2, dR2 = (t.cpu().numpy() for t in _run_gpu(x, dtype)[2])
+    for a, b in ((T, T2), (D, D2), (dR, dR2)):
+        np.testing.assert_array_equal(a[good], b[good])
