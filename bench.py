@@ -39,12 +39,13 @@ def kernel_source_hash(kernel="se_a"):
     return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
 
 
-def hbm_traffic(cfg_name, kernel, dtype="f64"):
-    """HBM bytes per launch, read from the committed rocprofv3 --pmc summary
-    (FETCH_SIZE and WRITE_SIZE, calibrated by a plain copy) if that summary
-    was taken on the current kernel source, with its file name; else
-    (None, None).  These counters cannot be read in the same process as the
-    timing, so the value is a stored measurement, not this run's."""
+def stored_profile(cfg_name, kernel, dtype="f64"):
+    """The committed rocprofv3 --pmc summary of this kernel and workload
+    (HBM bytes per launch from FETCH_SIZE and WRITE_SIZE, calibrated by a
+    plain copy; the shader clock from GRBM_GUI_ACTIVE where taken) and its
+    file name, if it was taken on the current kernel source; else (None,
+    None).  These counters cannot be read in the same process as the timing,
+    so the values are stored measurements, not this run's."""
     suffix = "" if dtype == "f64" else "_" + dtype
     rel = os.path.join("profiles", f"pmc_{kernel}_{cfg_name}{suffix}.json")
     p = os.path.join(ROOT, rel)
@@ -53,7 +54,12 @@ def hbm_traffic(cfg_name, kernel, dtype="f64"):
     d = json.load(open(p))
     if d.get("kernel_source_sha256_16") != kernel_source_hash(kernel):
         return None, None
-    return d.get("hbm_bytes_per_launch"), rel
+    return d, rel
+
+
+def hbm_traffic(cfg_name, kernel, dtype="f64"):
+    d, rel = stored_profile(cfg_name, kernel, dtype)
+    return (d.get("hbm_bytes_per_launch"), rel) if d else (None, None)
 
 
 def library_record():
@@ -68,9 +74,14 @@ def library_record():
 
 
 def roofline_entry(bound, kernel, achieved, peak, unit, cfg_name, dtype="f64", stored=True):
-    traffic, src = hbm_traffic(cfg_name, kernel, dtype) if stored else (None, None)
-    return {"bound": bound, "kernel": kernel, "achieved": achieved, "peak": peak, "unit": unit,
-            "frac": achieved / peak, "traffic": traffic, "traffic_source": src}
+    d, src = stored_profile(cfg_name, kernel, dtype) if stored else (None, None)
+    e = {"bound": bound, "kernel": kernel, "achieved": achieved, "peak": peak, "unit": unit,
+         "frac": achieved / peak, "traffic": d.get("hbm_bytes_per_launch") if d else None,
+         "traffic_source": src}
+    if d and d.get("shader_clock_ghz"):
+        # the peak is quoted at 2.4 GHz; the kernel ran at this clock under load
+        e["sclk_ghz"] = d["shader_clock_ghz"]
+    return e
 
 
 def cpu_baseline(x, seconds, dtype="f64", atoms=None):
