@@ -13,9 +13,10 @@
 //   1. zero the counters;  2. cell of each atom, counted with atomics;
 //   3. exclusive scan (one workgroup);  4. scatter the atoms into cell order
 //   with their coordinates, index and type packed in 32 bytes;
-//   5. one wavefront per atom walks the (up to) 27 cells around its own,
-//   64 candidates at a time, keeps those within r_c in LDS, ranks each of
-//   them among the candidates of its type and writes its slot.
+//   5. one wavefront per atom walks the (up to) 27 cells around its own as
+//   column spans of the cell-ordered array, 64 candidates at a time with
+//   the next batch in flight, keeps those within r_c in LDS, ranks each of
+//   them among the neighbours of its type and writes its slot.
 // The order inside a cell depends on the atomics, but the ranking is a total
 // order, so the list does not.
 #include <hip/hip_runtime.h>
@@ -31,7 +32,7 @@
 namespace {
 
 constexpr int kNlWaves = 4;      // wavefronts (atoms) per workgroup of the list kernel
-constexpr int kNlCap = 1024;     // neighbours within rc one wavefront keeps (16 KB of LDS)
+constexpr int kNlCap = 1024;     // neighbours within rc one wavefront keeps (12 KB of LDS)
 constexpr int kScanThreads = 1024;
 
 struct alignas(16) NlAtom {      // an atom in cell order
