@@ -9,7 +9,7 @@ Reading (the paper gives only the sizes): with x = D_i flattened row-major
     h_l = h_{l-1} + tanh(h_{l-1} W_l + b_l)    l = 2, 3 (equal widths: residual)
     E_i = h_3 . w_out + b_out,
 
-the same residual rule as the embedding net of this build.  The backward
+the same residual rule as the embedding net here.  The backward
 pass is the chain rule written out layer by layer (delta_l = dE/dh_l):
 
     delta_3 = w_out

@@ -4,8 +4,8 @@ Unlike ``synth.system`` these inputs come from no structure: every atom gets
 a random subset of its slots, and the first column of each valid row
 (s^ after normalisation) is placed in the four parts of the tabulation range
 in fixed shares (paper Sec. II: the table covers [s^(r_c), s^(r_l)] with an
-equal step; the extrapolation band and the clamp beyond it are this build's
-reading): below the lower end, in the main range, in the band, and past the
+equal step; the extrapolation band and the clamp beyond it are a reading
+where the paper is silent): below the lower end, in the main range, in the band, and past the
 band's end, plus rows exactly on the range's boundaries and on nodes.  The
 spatial columns are standard normal.  Only inputs are produced here.
 """

@@ -2,8 +2,8 @@
 
 The kernels' band and clamp paths are checked against the C oracle, so its
 ``locate`` must itself be pinned in all four parts (paper Sec. II: equal
-steps over [s^(r_c), s^(r_l)]; the band and the clamp are this build's
-reading): below the lower end (interval 0, t < 0), the main range, the
+steps over [s^(r_c), s^(r_l)]; the band and the clamp are a reading where
+the paper is silent): below the lower end (interval 0, t < 0), the main range, the
 extrapolation band and past its end (clamped: value at the end, zero
 derivative).  The numpy oracle's ``Table.locate`` is pinned on its own
 (closed forms, tabulation error in the band, the locate rules); here the C
