@@ -1,6 +1,6 @@
 """Piecewise fifth-order Hermite tabulation of the embedding net (oracle).
 
-Paper Sec. II ("Now, we describe the process to compress ..."): the input
+Paper Sec. II, the paragraph on the compression of the embedding net: the input
 range is cut into equal intervals of width Delta t; on [x_l, x_{l+1}) each
 channel m is replaced by
 
